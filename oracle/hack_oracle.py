@@ -445,7 +445,7 @@ def pack_cache(seqs, kv_heads: int, head_dim: int, bits: int, partition: int,
         for h in range(kv_heads):
             sq = seqs[s][h]
             L = sq.length
-            kbytes = pack_codes(sq.k_codes.reshape(L, P, Pi), bits).reshape(L, -1)
+            kbytes = pack_codes(sq.k_codes.reshape(L, P, Pi), bits).reshape(L, d * bits // 8)
             vbytes = pack_codes(np.transpose(sq.v_codes, (0, 2, 1)), bits)   # [NB][d][Pi*b/8]
             for t0 in range(0, L, page_tokens):
                 t1 = min(L, t0 + page_tokens)

@@ -1,0 +1,265 @@
+// C ABI of the library: argument validation on the host, then kernel launches
+// on the caller's stream.  Nothing here allocates device memory or synchronizes.
+#include <cstring>
+
+#include "hack_internal.hpp"
+
+using hack::CacheView;
+
+namespace {
+
+bool layout_ok(const hack_kv_layout* l) {
+  if (!l) return false;
+  const int pi = l->partition;
+  if (!(pi == 16 || pi == 32 || pi == 64 || pi == 128)) return false;
+  if (l->head_dim <= 0 || l->head_dim > 256 || l->head_dim % pi != 0) return false;
+  if (l->num_kv_heads < 1) return false;
+  if (!(l->kv_bits == 2 || l->kv_bits == 4)) return false;
+  if (l->page_tokens <= 0 || l->page_tokens % pi != 0) return false;
+  if (l->qp_bits != 8) return false;
+  if (!(l->rounding == HACK_ROUND_NEAREST_EVEN || l->rounding == HACK_ROUND_STOCHASTIC)) return false;
+  int need = l->kv_bits;
+  for (int v = 1; v < pi; v <<= 1) ++need;  // b + ceil(log2 pi)
+  return l->sum_bytes == (need <= 8 ? 1 : 2);
+}
+
+// Validates the cache pointers for `batch` sequences; returns the per-sequence capacity or -1.
+int64_t cache_capacity(const hack_kv_layout* l, const hack_kv_cache* c, int batch) {
+  if (!c) return -1;
+  if (!c->k_codes || !c->k_meta || !c->k_sums || !c->v_codes || !c->v_meta || !c->v_sums || !c->v_tail)
+    return -1;
+  if (c->num_pages <= 0) return -1;
+  if (c->block_table_dev) {
+    if (c->max_blocks_per_seq <= 0) return -1;
+    return (int64_t)c->max_blocks_per_seq * l->page_tokens;
+  }
+  if (c->num_pages < batch) return -1;
+  return l->page_tokens;
+}
+
+CacheView make_view(const hack_kv_layout* l, const hack_kv_cache* c) {
+  CacheView v;
+  v.k_codes = static_cast<uint8_t*>(c->k_codes);
+  v.k_meta = static_cast<__half2*>(c->k_meta);
+  v.k_sums = static_cast<uint8_t*>(c->k_sums);
+  v.v_codes = static_cast<uint8_t*>(c->v_codes);
+  v.v_meta = static_cast<__half2*>(c->v_meta);
+  v.v_sums = static_cast<uint8_t*>(c->v_sums);
+  v.v_tail = static_cast<__half*>(c->v_tail);
+  v.block_table = c->block_table_dev;
+  v.mbps = c->max_blocks_per_seq;
+  v.num_pages = c->num_pages;
+  v.page_tokens = l->page_tokens;
+  v.kv_heads = l->num_kv_heads;
+  v.head_dim = l->head_dim;
+  v.sum_bytes = l->sum_bytes;
+  return v;
+}
+
+hack_status from_hip(hipError_t e) { return e == hipSuccess ? HACK_OK : HACK_ERR_HIP; }
+
+// Shapes the attention kernels implement.
+hack_status attention_shape(const hack_kv_layout* l, int num_q_heads) {
+  if (num_q_heads < 1 || num_q_heads % l->num_kv_heads != 0) return HACK_ERR_INVALID_ARGUMENT;
+  if (l->head_dim != 128) return HACK_ERR_UNSUPPORTED;
+  if (!(l->partition == 32 || l->partition == 64)) return HACK_ERR_UNSUPPORTED;
+  if (num_q_heads / l->num_kv_heads > 8) return HACK_ERR_UNSUPPORTED;
+  return HACK_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+hack_status hack_kv_layout_make(hack_kv_layout* out, int32_t head_dim, int32_t num_kv_heads,
+                                int32_t kv_bits, int32_t partition, int32_t page_tokens,
+                                int32_t qp_bits, int32_t rounding, uint64_t seed) {
+  if (!out) return HACK_ERR_INVALID_ARGUMENT;
+  hack_kv_layout l;
+  std::memset(&l, 0, sizeof(l));
+  l.head_dim = head_dim;
+  l.num_kv_heads = num_kv_heads;
+  l.kv_bits = kv_bits;
+  l.partition = partition;
+  l.page_tokens = page_tokens;
+  l.qp_bits = qp_bits;
+  l.rounding = rounding;
+  l.seed = seed;
+  int need = kv_bits;
+  for (int v = 1; v < partition && v > 0; v <<= 1) ++need;
+  l.sum_bytes = need <= 8 ? 1 : 2;
+  if (!layout_ok(&l)) return HACK_ERR_INVALID_ARGUMENT;
+  *out = l;
+  return HACK_OK;
+}
+
+int64_t hack_kv_bytes(const hack_kv_layout* l, int64_t count, int32_t section) {
+  if (!layout_ok(l) || count < 0) return -1;
+  const int64_t d = l->head_dim, H = l->num_kv_heads, pt = l->page_tokens, pi = l->partition;
+  const int64_t P = d / pi;
+  switch (section) {
+    case HACK_K_CODES: return count * H * pt * (d * l->kv_bits / 8);
+    case HACK_K_META: return count * H * pt * P * 4;
+    case HACK_K_SUMS: return count * H * pt * P * l->sum_bytes;
+    case HACK_V_CODES: return count * H * (pt / pi) * d * (pi * l->kv_bits / 8);
+    case HACK_V_META: return count * H * (pt / pi) * d * 4;
+    case HACK_V_SUMS: return count * H * (pt / pi) * d * l->sum_bytes;
+    case HACK_V_TAIL: return count * H * pi * d * 2;
+    default: return -1;
+  }
+}
+
+hack_status hack_quantize(const hack_kv_layout* layout, const hack_kv_cache* cache, const void* k_dev,
+                          const void* v_dev, const int32_t* seq_lens_dev, int32_t batch, int32_t max_len,
+                          hipStream_t stream) {
+  if (!layout_ok(layout) || !k_dev || !v_dev || !seq_lens_dev || batch < 0 || max_len < 0)
+    return HACK_ERR_INVALID_ARGUMENT;
+  const int64_t cap = cache_capacity(layout, cache, batch);
+  if (cap < 0) return HACK_ERR_INVALID_ARGUMENT;
+  if (max_len > cap) return HACK_ERR_CAPACITY;
+  if (batch == 0 || max_len == 0) return HACK_OK;
+  (void)hipGetLastError();
+  return from_hip(hack::launch_quantize(*layout, make_view(layout, cache), static_cast<const __half*>(k_dev),
+                                        static_cast<const __half*>(v_dev), seq_lens_dev, batch, max_len, stream));
+}
+
+hack_status hack_append(const hack_kv_layout* layout, const hack_kv_cache* cache, const void* k_new_dev,
+                        const void* v_new_dev, int32_t* seq_lens_dev, int32_t batch, int32_t max_len,
+                        int32_t tail_mode, hipStream_t stream) {
+  if (!layout_ok(layout) || !k_new_dev || !v_new_dev || !seq_lens_dev || batch < 0 || max_len < 0)
+    return HACK_ERR_INVALID_ARGUMENT;
+  if (!(tail_mode == HACK_TAIL_FP16 || tail_mode == HACK_TAIL_REQUANT)) return HACK_ERR_INVALID_ARGUMENT;
+  const int64_t cap = cache_capacity(layout, cache, batch);
+  if (cap < 0) return HACK_ERR_INVALID_ARGUMENT;
+  if ((int64_t)max_len + 1 > cap) return HACK_ERR_CAPACITY;
+  if (batch == 0) return HACK_OK;
+  (void)hipGetLastError();
+  return from_hip(hack::launch_append(*layout, make_view(layout, cache), static_cast<const __half*>(k_new_dev),
+                                      static_cast<const __half*>(v_new_dev), seq_lens_dev, batch, (int)cap,
+                                      tail_mode == HACK_TAIL_REQUANT, stream));
+}
+
+int64_t hack_decode_workspace_bytes(const hack_kv_layout* layout, int32_t batch, int32_t num_q_heads,
+                                    int32_t max_len) {
+  if (!layout_ok(layout) || batch < 0 || max_len < 0 || num_q_heads < 1 ||
+      num_q_heads % layout->num_kv_heads != 0)
+    return -1;
+  return hack::plan_decode(*layout, batch, num_q_heads, max_len).workspace_bytes;
+}
+
+static hack_status decode_common(const hack_kv_layout* layout, const hack_kv_cache* cache, const void* q_dev,
+                                 int32_t num_q_heads, const int32_t* seq_lens_dev, int32_t batch,
+                                 int32_t max_len, hack::DecodeArgs& a, int64_t* cap_out) {
+  if (!layout_ok(layout) || !q_dev || !seq_lens_dev || batch < 0 || max_len < 0)
+    return HACK_ERR_INVALID_ARGUMENT;
+  const hack_status sh = attention_shape(layout, num_q_heads);
+  if (sh != HACK_OK) return sh;
+  const int64_t cap = cache_capacity(layout, cache, batch);
+  if (cap < 0) return HACK_ERR_INVALID_ARGUMENT;
+  if (max_len > cap) return HACK_ERR_CAPACITY;
+  std::memset(&a, 0, sizeof(a));
+  a.c = make_view(layout, cache);
+  a.q = static_cast<const __half*>(q_dev);
+  a.lens = seq_lens_dev;
+  a.num_q_heads = num_q_heads;
+  a.group = num_q_heads / layout->num_kv_heads;
+  a.max_len = max_len;
+  *cap_out = cap;
+  return HACK_OK;
+}
+
+hack_status hack_attend_decode(const hack_kv_layout* layout, const hack_kv_cache* cache, const void* q_dev,
+                               int32_t num_q_heads, const int32_t* seq_lens_dev, int32_t batch, int32_t max_len,
+                               int32_t tail_mode, float* out_dev, void* workspace_dev, int64_t workspace_bytes,
+                               hipStream_t stream) {
+  hack::DecodeArgs a;
+  int64_t cap = 0;
+  hack_status st = decode_common(layout, cache, q_dev, num_q_heads, seq_lens_dev, batch, max_len, a, &cap);
+  if (st != HACK_OK) return st;
+  if (!out_dev || !(tail_mode == HACK_TAIL_FP16 || tail_mode == HACK_TAIL_REQUANT))
+    return HACK_ERR_INVALID_ARGUMENT;
+  const hack::DecodePlan plan = hack::plan_decode(*layout, batch, num_q_heads, max_len);
+  if (!workspace_dev || workspace_bytes < plan.workspace_bytes) return HACK_ERR_WORKSPACE;
+  if (batch == 0) return HACK_OK;
+  a.out = out_dev;
+  a.partials = static_cast<float*>(workspace_dev);
+  a.counters = reinterpret_cast<int32_t*>(static_cast<uint8_t*>(workspace_dev) + plan.counter_offset);
+  a.chunk = plan.chunk;
+  a.splits = plan.splits;
+  a.tail_requant = tail_mode == HACK_TAIL_REQUANT;
+  (void)hipGetLastError();
+  return from_hip(hack::launch_decode(*layout, a, batch, hack::MODE_ATTEND, stream));
+}
+
+hack_status hack_attend_prefill(const hack_kv_layout* layout, const hack_kv_cache* cache, const void* q_dev,
+                                int32_t num_q_heads, int32_t batch, int32_t len, int32_t causal, float* out_dev,
+                                hipStream_t stream) {
+  if (!layout_ok(layout) || !q_dev || !out_dev || batch < 0 || len < 0) return HACK_ERR_INVALID_ARGUMENT;
+  const hack_status sh = attention_shape(layout, num_q_heads);
+  if (sh != HACK_OK) return sh;
+  const int64_t cap = cache_capacity(layout, cache, batch);
+  if (cap < 0) return HACK_ERR_INVALID_ARGUMENT;
+  if (len > cap) return HACK_ERR_CAPACITY;
+  if (batch == 0 || len == 0) return HACK_OK;
+  (void)hipGetLastError();
+  return from_hip(hack::launch_prefill(*layout, make_view(layout, cache), static_cast<const __half*>(q_dev),
+                                       num_q_heads, batch, len, causal != 0, out_dev, stream));
+}
+
+const char* hack_status_string(hack_status status) {
+  switch (status) {
+    case HACK_OK: return "ok";
+    case HACK_ERR_INVALID_ARGUMENT: return "invalid argument";
+    case HACK_ERR_UNSUPPORTED: return "unsupported format or shape";
+    case HACK_ERR_CAPACITY: return "length exceeds the cache capacity";
+    case HACK_ERR_WORKSPACE: return "workspace missing or too small";
+    case HACK_ERR_HIP: return "HIP launch failure";
+    default: return "unknown status";
+  }
+}
+
+hack_status hack_debug_qk_products(const hack_kv_layout* layout, const hack_kv_cache* cache, const void* q_dev,
+                                   int32_t num_q_heads, const int32_t* seq_lens_dev, int32_t batch,
+                                   int32_t max_len, uint8_t* q_codes_dev, float* q_meta_dev,
+                                   int32_t* products_dev, hipStream_t stream) {
+  hack::DecodeArgs a;
+  int64_t cap = 0;
+  hack_status st = decode_common(layout, cache, q_dev, num_q_heads, seq_lens_dev, batch, max_len, a, &cap);
+  if (st != HACK_OK) return st;
+  if (!q_codes_dev || !q_meta_dev || !products_dev) return HACK_ERR_INVALID_ARGUMENT;
+  if (batch == 0) return HACK_OK;
+  const hack::DecodePlan plan = hack::plan_decode(*layout, batch, num_q_heads, max_len);
+  a.chunk = plan.chunk;
+  a.splits = plan.splits;
+  a.dbg_qcodes = q_codes_dev;
+  a.dbg_qmeta = q_meta_dev;
+  a.dbg_prod = products_dev;
+  (void)hipGetLastError();
+  return from_hip(hack::launch_decode(*layout, a, batch, hack::MODE_QK, stream));
+}
+
+hack_status hack_debug_pv_products(const hack_kv_layout* layout, const hack_kv_cache* cache,
+                                   const uint8_t* p_codes_dev, const float* p_meta_dev, int32_t num_q_heads,
+                                   const int32_t* seq_lens_dev, int32_t batch, int32_t max_len,
+                                   int32_t* products_dev, float* out_dev, hipStream_t stream) {
+  hack::DecodeArgs a;
+  int64_t cap = 0;
+  // the query is not read in this mode; pass any non-null pointer through validation
+  hack_status st = decode_common(layout, cache, p_codes_dev, num_q_heads, seq_lens_dev, batch, max_len, a, &cap);
+  if (st != HACK_OK) return st;
+  if (!p_meta_dev || !products_dev || !out_dev) return HACK_ERR_INVALID_ARGUMENT;
+  if (batch == 0) return HACK_OK;
+  const int span = 4 * layout->partition;
+  a.q = nullptr;
+  a.chunk = ((max_len + span - 1) / span) * span;
+  if (a.chunk == 0) a.chunk = span;
+  a.splits = 1;
+  a.out = out_dev;
+  a.dbg_prod = products_dev;
+  a.dbg_pcodes = p_codes_dev;
+  a.dbg_pmeta = p_meta_dev;
+  (void)hipGetLastError();
+  return from_hip(hack::launch_decode(*layout, a, batch, hack::MODE_PV, stream));
+}
+
+}  // extern "C"

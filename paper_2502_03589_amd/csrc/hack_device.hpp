@@ -1,0 +1,181 @@
+// Device-side helpers of the HIP kernels: cache addressing, the partition
+// quantizer (Sec. 5.2) in a pinned float32 operation order, and cross-lane
+// reductions.  Everything here is compiled for gfx950 only.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <hip/hip_fp16.h>
+#include <stdint.h>
+
+namespace hack {
+
+// Geometry and device pointers of one cache (see the section layout in hack.h).
+struct CacheView {
+  uint8_t* k_codes;
+  __half2* k_meta;
+  uint8_t* k_sums;
+  uint8_t* v_codes;
+  __half2* v_meta;
+  uint8_t* v_sums;
+  __half* v_tail;
+  const int32_t* block_table;  // [batch][mbps] or nullptr
+  int mbps;                    // max blocks per sequence
+  int64_t num_pages;
+  int page_tokens;
+  int kv_heads;
+  int head_dim;
+  int sum_bytes;
+};
+
+// Page of token t of sequence s (a contiguous cache maps sequence s to page s).
+// A page index outside [0, num_pages) is clamped: a bad table gives wrong values,
+// never an access outside the cache.
+__device__ __forceinline__ int64_t page_of(const CacheView& c, int s, int t) {
+  int64_t pg = c.block_table ? (int64_t)c.block_table[(int64_t)s * c.mbps + t / c.page_tokens] : (int64_t)s;
+  return pg < 0 ? 0 : (pg >= c.num_pages ? c.num_pages - 1 : pg);
+}
+
+// Row index of token t's K data: ((page * H + h) * page_tokens + slot).
+__device__ __forceinline__ int64_t k_row(const CacheView& c, int s, int h, int t) {
+  return (page_of(c, s, t) * c.kv_heads + h) * c.page_tokens + (t % c.page_tokens);
+}
+
+// Index of the V block holding token t: ((page * H + h) * page_tokens/PI + block-in-page).
+template <int PI>
+__device__ __forceinline__ int64_t v_block(const CacheView& c, int s, int h, int t) {
+  return (page_of(c, s, t) * c.kv_heads + h) * (c.page_tokens / PI) + (t % c.page_tokens) / PI;
+}
+
+__device__ __forceinline__ uint32_t load_sum(const uint8_t* base, int64_t idx, int sum_bytes) {
+  return sum_bytes == 1 ? (uint32_t)base[idx] : (uint32_t)reinterpret_cast<const uint16_t*>(base)[idx];
+}
+
+__device__ __forceinline__ void store_sum(uint8_t* base, int64_t idx, int sum_bytes, uint32_t v) {
+  if (sum_bytes == 1) base[idx] = (uint8_t)v;
+  else reinterpret_cast<uint16_t*>(base)[idx] = (uint16_t)v;
+}
+
+// ---------------------------------------------------------------------------
+// Stochastic-rounding thresholds: SplitMix64 (Steele, Lea and Flood, 2014).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint64_t splitmix64(uint64_t x) {
+  uint64_t z = x + 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+// u in [0, 1): the top 24 bits of SplitMix64(key ^ idx) scaled by 2^-24.
+__device__ __forceinline__ float sr_threshold(uint64_t key, uint64_t idx) {
+  return (float)(uint32_t)(splitmix64(key ^ idx) >> 40) * 5.9604644775390625e-08f;
+}
+
+// Smallest fp16 value >= s (s >= 0, finite), as raw bits.
+__device__ __forceinline__ uint16_t half_bits_round_up(float s) {
+  __half h = __float2half_rn(s);
+  uint16_t bits = __half_as_ushort(h);
+  if (__half2float(h) < s) bits = (uint16_t)(bits + 1);
+  return bits;
+}
+
+// Quantize the first `n` of N values as one partition (Sec. 5.2):
+//   m = min, s = fp16_round_up(fl(fl(max - m) / (2^b - 1))), r = fl(1/s),
+//   t = fl(fl(x - m) * r), code = min(2^b - 1, round(t)) (nearest-even, or stochastic
+//   with threshold u: floor(t) + [u < t - floor(t)]); s == 0 gives all-zero codes.
+// Codes are packed LSB-first into `words` (element e at bit e*BITS); elements past n
+// get code 0.  Returns the code sum; writes (m, s) as raw fp16 bits.
+template <int BITS, int N>
+__device__ __forceinline__ uint32_t quantize_values(const float (&x)[N], int n, bool stochastic,
+                                                    uint64_t key, uint64_t idx0, uint64_t idx_step,
+                                                    uint32_t (&words)[(N * BITS + 31) / 32],
+                                                    uint16_t& m_bits, uint16_t& s_bits) {
+#pragma clang fp contract(off)
+  constexpr float QMAX = (float)((1 << BITS) - 1);
+  float mn = x[0], mx = x[0];
+#pragma unroll
+  for (int e = 1; e < N; ++e) {
+    if (e < n) {
+      mn = fminf(mn, x[e]);
+      mx = fmaxf(mx, x[e]);
+    }
+  }
+  const float s32 = __fdiv_rn(__fsub_rn(mx, mn), QMAX);
+  s_bits = half_bits_round_up(s32);
+  m_bits = __half_as_ushort(__float2half_rn(mn));  // exact: m is an fp16 input value
+  const float s = __half2float(__ushort_as_half(s_bits));
+#pragma unroll
+  for (int w = 0; w < (N * BITS + 31) / 32; ++w) words[w] = 0u;
+  uint32_t sum = 0;
+  if (s != 0.0f) {
+    const float r = __fdiv_rn(1.0f, s);
+#pragma unroll
+    for (int e = 0; e < N; ++e) {
+      if (e < n) {
+        const float t = __fmul_rn(__fsub_rn(x[e], mn), r);
+        float c;
+        if (!stochastic) {
+          c = rintf(t);
+        } else {
+          const float fl = floorf(t);
+          const float u = sr_threshold(key, idx0 + (uint64_t)e * idx_step);
+          c = fl + ((u < __fsub_rn(t, fl)) ? 1.0f : 0.0f);
+        }
+        c = fminf(c, QMAX);
+        const uint32_t ci = (uint32_t)c;
+        words[(e * BITS) / 32] |= ci << ((e * BITS) % 32);
+        sum += ci;
+      }
+    }
+  }
+  return sum;
+}
+
+// Canonical element index used for stochastic thresholds:
+// ((seq * H_kv + head) * 2^32 + token) * d + channel.
+__device__ __forceinline__ uint64_t element_index(int s, int kv_heads, int h, int t, int d, int ch) {
+  return ((((uint64_t)(s * kv_heads + h)) << 32) + (uint64_t)t) * (uint64_t)d + (uint64_t)ch;
+}
+
+// ---------------------------------------------------------------------------
+// Cross-lane reductions inside a row of 16 lanes (DPP row rotates).
+// ---------------------------------------------------------------------------
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int x) {
+  return __builtin_amdgcn_mov_dpp(x, CTRL, 0xF, 0xF, false);
+}
+
+// row_ror:n has DPP control 0x120 + n.
+__device__ __forceinline__ float row16_max(float x) {
+  x = fmaxf(x, dpp_f<0x128>(x));
+  x = fmaxf(x, dpp_f<0x124>(x));
+  x = fmaxf(x, dpp_f<0x122>(x));
+  x = fmaxf(x, dpp_f<0x121>(x));
+  return x;
+}
+__device__ __forceinline__ float row16_min(float x) {
+  x = fminf(x, dpp_f<0x128>(x));
+  x = fminf(x, dpp_f<0x124>(x));
+  x = fminf(x, dpp_f<0x122>(x));
+  x = fminf(x, dpp_f<0x121>(x));
+  return x;
+}
+__device__ __forceinline__ float row16_sum(float x) {
+  x += dpp_f<0x128>(x);
+  x += dpp_f<0x124>(x);
+  x += dpp_f<0x122>(x);
+  x += dpp_f<0x121>(x);
+  return x;
+}
+__device__ __forceinline__ int row16_sum_i(int x) {
+  x += dpp_i<0x128>(x);
+  x += dpp_i<0x124>(x);
+  x += dpp_i<0x122>(x);
+  x += dpp_i<0x121>(x);
+  return x;
+}
+
+}  // namespace hack

@@ -1,0 +1,64 @@
+// Launchers shared between the C-ABI layer (hack_api.hip) and the kernel files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <hip/hip_fp16.h>
+#include <stdint.h>
+
+#include "../../include/hack.h"
+#include "hack_device.hpp"
+
+namespace hack {
+
+// Decode split plan: tokens per workgroup (a multiple of 4*partition) and the
+// number of splits of the longest sequence.  Depends only on the sizes, so the
+// workspace query and the attend call always agree.
+struct DecodePlan {
+  int chunk;
+  int splits;
+  int64_t partial_floats;   // batch * H_kv * splits * G * (2 + head_dim)
+  int64_t counter_offset;   // byte offset of the int32 counters in the workspace
+  int64_t workspace_bytes;
+};
+
+DecodePlan plan_decode(const hack_kv_layout& lay, int batch, int num_q_heads, int max_len);
+
+hipError_t launch_quantize(const hack_kv_layout& lay, const CacheView& c, const __half* k,
+                           const __half* v, const int32_t* lens, int batch, int max_len,
+                           hipStream_t stream);
+
+hipError_t launch_append(const hack_kv_layout& lay, const CacheView& c, const __half* k_new,
+                         const __half* v_new, int32_t* lens, int batch, int capacity,
+                         int tail_requant, hipStream_t stream);
+
+enum DecodeMode { MODE_ATTEND = 0, MODE_QK = 1, MODE_PV = 2 };
+
+struct DecodeArgs {
+  CacheView c;
+  const __half* q;        // [B][H_q][128]
+  const int32_t* lens;    // [B]
+  float* out;             // [B][H_q][128]
+  float* partials;        // [B][H_kv][splits][G][2 + 128]
+  int32_t* counters;      // [B][H_kv]
+  int num_q_heads;
+  int group;              // H_q / H_kv
+  int chunk;
+  int splits;
+  int tail_requant;
+  int max_len;
+  // test exports
+  uint8_t* dbg_qcodes;    // [B][H_q][128]
+  float* dbg_qmeta;       // [B][H_q][P][2]
+  int32_t* dbg_prod;      // QK: [B][H_q][max_len][P]; PV: [B][H_q][NB][128]
+  const uint8_t* dbg_pcodes;  // [B][H_q][NB][PI]
+  const float* dbg_pmeta;     // [B][H_q][NB][2]
+};
+
+hipError_t launch_decode(const hack_kv_layout& lay, const DecodeArgs& a, int batch, int mode,
+                         hipStream_t stream);
+
+hipError_t launch_prefill(const hack_kv_layout& lay, const CacheView& c, const __half* q,
+                          int num_q_heads, int batch, int len, int causal, float* out,
+                          hipStream_t stream);
+
+}  // namespace hack

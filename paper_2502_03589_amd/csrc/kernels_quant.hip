@@ -1,0 +1,209 @@
+// Quantize-on-write kernels (Sec. 5.1 steps 2 and 9; Sec. 5.2 quantizer; Sec. 5.3
+// partitioning and the fp16 open V block).
+//   quantize_k: one thread per (sequence, kv head, token, K partition along d)
+//   quantize_v: one thread per (sequence, kv head, V block, channel)
+//   append    : one workgroup per sequence, one new token for every kv head
+// All are HBM-bound: they read fp16 values once and write codes, (min, scale) and sums.
+#include "hack_internal.hpp"
+
+namespace hack {
+
+template <int PI>
+__device__ __forceinline__ void load_f16_run(const __half* __restrict__ src, float (&x)[PI]) {
+  // PI contiguous fp16 values, 16 bytes at a time (PI is a multiple of 16).
+  const uint4* p = reinterpret_cast<const uint4*>(src);
+#pragma unroll
+  for (int i = 0; i < PI / 8; ++i) {
+    uint4 w = p[i];
+    const __half2* h = reinterpret_cast<const __half2*>(&w);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      float2 f = __half22float2(h[j]);
+      x[8 * i + 2 * j] = f.x;
+      x[8 * i + 2 * j + 1] = f.y;
+    }
+  }
+}
+
+template <int BITS, int PI>
+__device__ __forceinline__ void store_codes(uint8_t* dst, const uint32_t (&w)[(PI * BITS + 31) / 32]) {
+  uint32_t* d = reinterpret_cast<uint32_t*>(dst);
+#pragma unroll
+  for (int i = 0; i < (PI * BITS + 31) / 32; ++i) d[i] = w[i];
+}
+
+template <int BITS, int PI>
+__global__ __launch_bounds__(256) void quantize_k_kernel(CacheView c, const __half* __restrict__ k,
+                                                         const int32_t* __restrict__ lens, int batch,
+                                                         int max_len, int stochastic, uint64_t key) {
+  const int P = c.head_dim / PI;
+  const int64_t total = (int64_t)batch * c.kv_heads * max_len * P;
+  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (gid >= total) return;
+  const int p = (int)(gid % P);
+  int64_t r = gid / P;
+  const int t = (int)(r % max_len);
+  r /= max_len;
+  const int h = (int)(r % c.kv_heads);
+  const int s = (int)(r / c.kv_heads);
+  if (t >= min(lens[s], max_len)) return;
+  float x[PI];
+  load_f16_run<PI>(k + (((int64_t)s * c.kv_heads + h) * max_len + t) * c.head_dim + p * PI, x);
+  uint32_t w[(PI * BITS + 31) / 32];
+  uint16_t mb, sb;
+  const uint32_t sum = quantize_values<BITS, PI>(
+      x, PI, stochastic != 0, key, element_index(s, c.kv_heads, h, t, c.head_dim, p * PI), 1ull, w, mb, sb);
+  const int64_t row = k_row(c, s, h, t);
+  store_codes<BITS, PI>(c.k_codes + row * (c.head_dim * BITS / 8) + p * (PI * BITS / 8), w);
+  reinterpret_cast<uint32_t*>(c.k_meta)[row * P + p] = (uint32_t)mb | ((uint32_t)sb << 16);
+  store_sum(c.k_sums, row * P + p, c.sum_bytes, sum);
+}
+
+template <int BITS, int PI>
+__global__ __launch_bounds__(256) void quantize_v_kernel(CacheView c, const __half* __restrict__ v,
+                                                         const int32_t* __restrict__ lens, int batch,
+                                                         int max_len, int stochastic, uint64_t key) {
+  const int d = c.head_dim;
+  const int NB = (max_len + PI - 1) / PI;
+  const int64_t total = (int64_t)batch * c.kv_heads * NB * d;
+  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (gid >= total) return;
+  const int ch = (int)(gid % d);
+  int64_t r = gid / d;
+  const int blk = (int)(r % NB);
+  r /= NB;
+  const int h = (int)(r % c.kv_heads);
+  const int s = (int)(r / c.kv_heads);
+  const int L = max(0, min(lens[s], max_len));  // lengths past max_len are ignored
+  const int F = L / PI, T = L - F * PI;
+  if (blk > F || (blk == F && T == 0)) return;
+  const int n = blk < F ? PI : T;
+  const __half* src = v + (((int64_t)s * c.kv_heads + h) * max_len + (int64_t)blk * PI) * d + ch;
+  float x[PI];
+#pragma unroll
+  for (int e = 0; e < PI; ++e) x[e] = e < n ? __half2float(src[(int64_t)e * d]) : 0.0f;
+  uint32_t w[(PI * BITS + 31) / 32];
+  uint16_t mb, sb;
+  const uint32_t sum = quantize_values<BITS, PI>(
+      x, n, stochastic != 0, key, element_index(s, c.kv_heads, h, blk * PI, d, ch), (uint64_t)d, w, mb, sb);
+  const int64_t vb = v_block<PI>(c, s, h, blk * PI);
+  store_codes<BITS, PI>(c.v_codes + (vb * d + ch) * (PI * BITS / 8), w);
+  reinterpret_cast<uint32_t*>(c.v_meta)[vb * d + ch] = (uint32_t)mb | ((uint32_t)sb << 16);
+  store_sum(c.v_sums, vb * d + ch, c.sum_bytes, sum);
+  if (blk == F) {  // the open block: keep its fp16 originals
+    __half* tail = c.v_tail + (((int64_t)s * c.kv_heads + h) * PI) * d + ch;
+    for (int e = 0; e < T; ++e) tail[(int64_t)e * d] = src[(int64_t)e * d];
+  }
+}
+
+// One new token per sequence: K partitions of the token; V value into the fp16
+// open block, which is quantized when it fills (and on every call in REQUANT mode).
+template <int BITS, int PI>
+__global__ __launch_bounds__(256) void append_kernel(CacheView c, const __half* __restrict__ k_new,
+                                                     const __half* __restrict__ v_new, int32_t* lens,
+                                                     int capacity, int requant, int stochastic,
+                                                     uint64_t key_k, uint64_t key_v) {
+  __shared__ int s_len;
+  const int s = blockIdx.x;
+  if (threadIdx.x == 0) s_len = lens[s];
+  __syncthreads();
+  const int L = s_len;
+  if (L < 0 || L >= capacity) return;  // uniform across the workgroup
+  const int H = c.kv_heads, d = c.head_dim, P = d / PI;
+  for (int w = threadIdx.x; w < H * P; w += blockDim.x) {
+    const int h = w / P, p = w % P;
+    float x[PI];
+    load_f16_run<PI>(k_new + ((int64_t)s * H + h) * d + p * PI, x);
+    uint32_t words[(PI * BITS + 31) / 32];
+    uint16_t mb, sb;
+    const uint32_t sum = quantize_values<BITS, PI>(
+        x, PI, stochastic != 0, key_k, element_index(s, H, h, L, d, p * PI), 1ull, words, mb, sb);
+    const int64_t row = k_row(c, s, h, L);
+    store_codes<BITS, PI>(c.k_codes + row * (d * BITS / 8) + p * (PI * BITS / 8), words);
+    reinterpret_cast<uint32_t*>(c.k_meta)[row * P + p] = (uint32_t)mb | ((uint32_t)sb << 16);
+    store_sum(c.k_sums, row * P + p, c.sum_bytes, sum);
+  }
+  const int F = L / PI, T = L - F * PI;  // the new token is element T of block F
+  for (int w = threadIdx.x; w < H * d; w += blockDim.x) {
+    const int h = w / d, ch = w % d;
+    const __half vn = v_new[((int64_t)s * H + h) * d + ch];
+    __half* tail = c.v_tail + (((int64_t)s * H + h) * PI) * d + ch;
+    tail[(int64_t)T * d] = vn;
+    const int n = T + 1;
+    if (n == PI || requant) {
+      float x[PI];
+#pragma unroll
+      for (int e = 0; e < PI; ++e)
+        x[e] = e < T ? __half2float(tail[(int64_t)e * d]) : (e == T ? __half2float(vn) : 0.0f);
+      uint32_t words[(PI * BITS + 31) / 32];
+      uint16_t mb, sb;
+      const uint32_t sum = quantize_values<BITS, PI>(
+          x, n, stochastic != 0, key_v, element_index(s, H, h, F * PI, d, ch), (uint64_t)d, words, mb, sb);
+      const int64_t vb = v_block<PI>(c, s, h, F * PI);
+      store_codes<BITS, PI>(c.v_codes + (vb * d + ch) * (PI * BITS / 8), words);
+      reinterpret_cast<uint32_t*>(c.v_meta)[vb * d + ch] = (uint32_t)mb | ((uint32_t)sb << 16);
+      store_sum(c.v_sums, vb * d + ch, c.sum_bytes, sum);
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) lens[s] = L + 1;
+}
+
+static uint64_t stream_key(uint64_t seed, uint64_t stream) { return seed ^ (stream << 56); }
+
+template <int BITS, int PI>
+static hipError_t quantize_impl(const hack_kv_layout& lay, const CacheView& c, const __half* k,
+                                const __half* v, const int32_t* lens, int batch, int max_len,
+                                hipStream_t stream) {
+  const int stoch = lay.rounding == HACK_ROUND_STOCHASTIC;
+  const int64_t nk = (int64_t)batch * c.kv_heads * max_len * (c.head_dim / PI);
+  if (nk > 0)
+    hipLaunchKernelGGL((quantize_k_kernel<BITS, PI>), dim3((unsigned)((nk + 255) / 256)), dim3(256), 0,
+                       stream, c, k, lens, batch, max_len, stoch, stream_key(lay.seed, 1));
+  const int64_t nv = (int64_t)batch * c.kv_heads * ((max_len + PI - 1) / PI) * c.head_dim;
+  if (nv > 0)
+    hipLaunchKernelGGL((quantize_v_kernel<BITS, PI>), dim3((unsigned)((nv + 255) / 256)), dim3(256), 0,
+                       stream, c, v, lens, batch, max_len, stoch, stream_key(lay.seed, 2));
+  return hipGetLastError();
+}
+
+template <int BITS, int PI>
+static hipError_t append_impl(const hack_kv_layout& lay, const CacheView& c, const __half* k_new,
+                              const __half* v_new, int32_t* lens, int batch, int capacity,
+                              int tail_requant, hipStream_t stream) {
+  const int stoch = lay.rounding == HACK_ROUND_STOCHASTIC;
+  hipLaunchKernelGGL((append_kernel<BITS, PI>), dim3(batch), dim3(256), 0, stream, c, k_new, v_new, lens,
+                     capacity, tail_requant, stoch, stream_key(lay.seed, 1), stream_key(lay.seed, 2));
+  return hipGetLastError();
+}
+
+#define HACK_DISPATCH_BITS_PI(BITS_, PI_, CALL)                        \
+  switch ((BITS_) * 1000 + (PI_)) {                                    \
+    case 2016: return CALL(2, 16);                                     \
+    case 2032: return CALL(2, 32);                                     \
+    case 2064: return CALL(2, 64);                                     \
+    case 2128: return CALL(2, 128);                                    \
+    case 4016: return CALL(4, 16);                                     \
+    case 4032: return CALL(4, 32);                                     \
+    case 4064: return CALL(4, 64);                                     \
+    case 4128: return CALL(4, 128);                                    \
+    default: return hipErrorInvalidValue;                              \
+  }
+
+hipError_t launch_quantize(const hack_kv_layout& lay, const CacheView& c, const __half* k,
+                           const __half* v, const int32_t* lens, int batch, int max_len,
+                           hipStream_t stream) {
+#define CALLQ(B, P) quantize_impl<B, P>(lay, c, k, v, lens, batch, max_len, stream)
+  HACK_DISPATCH_BITS_PI(lay.kv_bits, lay.partition, CALLQ)
+#undef CALLQ
+}
+
+hipError_t launch_append(const hack_kv_layout& lay, const CacheView& c, const __half* k_new,
+                         const __half* v_new, int32_t* lens, int batch, int capacity,
+                         int tail_requant, hipStream_t stream) {
+#define CALLA(B, P) append_impl<B, P>(lay, c, k_new, v_new, lens, batch, capacity, tail_requant, stream)
+  HACK_DISPATCH_BITS_PI(lay.kv_bits, lay.partition, CALLA)
+#undef CALLA
+}
+
+}  // namespace hack

@@ -1,0 +1,149 @@
+"""Host-only checks of the C ABI: the library loads, exports every function that
+include/hack.h declares, and rejects bad arguments before launching anything.
+No call here reaches the GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from oracle import hack_oracle as O
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "hack.h")
+
+hk = pytest.importorskip("paper_2502_03589_amd.hack")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(hk.library_path()):
+        pytest.skip("libhack.so not built (run __graft_entry__.build())")
+    return hk.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(hack_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared_functions()
+    assert len(names) >= 10
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(hk.EXPORTS)
+
+
+def test_layout_make_validation(lib):
+    good = hk.hack_kv_layout_make(128, 8, 2, 32, 256)
+    assert good.sum_bytes == 1 and good.qp_bits == 8
+    assert hk.hack_kv_layout_make(128, 8, 2, 128, 256).sum_bytes == 2     # 9-bit sums -> 2 bytes
+    assert hk.hack_kv_layout_make(128, 8, 4, 64, 256).sum_bytes == 2
+    bad = [
+        (128, 8, 3, 32, 256), (128, 8, 8, 32, 256), (128, 8, 2, 48, 256), (100, 8, 2, 32, 256),
+        (128, 0, 2, 32, 256), (128, 8, 2, 32, 100), (128, 8, 2, 32, 0), (512, 8, 2, 32, 256),
+    ]
+    for args in bad:
+        with pytest.raises(hk.HackError) as e:
+            hk.hack_kv_layout_make(*args)
+        assert e.value.status == 1
+    with pytest.raises(hk.HackError):
+        hk.hack_kv_layout_make(128, 8, 2, 32, 256, qp_bits=4)
+    with pytest.raises(hk.HackError):
+        hk.hack_kv_layout_make(128, 8, 2, 32, 256, rounding=7)
+    assert lib.hack_kv_layout_make(None, 128, 8, 2, 32, 256, 8, 0, 0) == 1
+
+
+@pytest.mark.parametrize("bits,pi", [(2, 32), (4, 32), (2, 64), (4, 64), (2, 128), (2, 16)])
+def test_section_sizes_closed_form(lib, bits, pi):
+    d, H, pt, pages = 128, 8, 256, 5
+    lay = hk.hack_kv_layout_make(d, H, bits, pi, pt)
+    P = d // pi
+    sb = O.sum_bytes(bits, pi)
+    expect = {
+        hk.K_CODES: pages * H * pt * d * bits // 8,
+        hk.K_META: pages * H * pt * P * 4,
+        hk.K_SUMS: pages * H * pt * P * sb,
+        hk.V_CODES: pages * H * (pt // pi) * d * pi * bits // 8,
+        hk.V_META: pages * H * (pt // pi) * d * 4,
+        hk.V_SUMS: pages * H * (pt // pi) * d * sb,
+    }
+    for sec, n in expect.items():
+        assert hk.hack_kv_bytes(lay, pages, sec) == n
+    assert hk.hack_kv_bytes(lay, 3, hk.V_TAIL) == 3 * H * pi * d * 2
+    assert hk.hack_kv_bytes(lay, -1, hk.K_CODES) == -1
+    assert hk.hack_kv_bytes(lay, 1, 99) == -1
+    # bytes per token per kv head (K + V, excluding the fp16 open block): b=2, pi=32 -> 104
+    per_tok = sum(hk.hack_kv_bytes(lay, 1, s) for s in range(6)) / (H * pt)
+    assert per_tok == (d * bits // 8 + P * (4 + sb)) + d * (pi * bits // 8 + 4 + sb) / pi
+
+
+def test_compression_ratio_of_format(lib):
+    """Sec. 7.2: codes + fp16 min/scale at 2 bits and Pi = 64 are ~15% of fp16 KV."""
+    lay = hk.hack_kv_layout_make(128, 1, 2, 64, 64)
+    codes_meta = sum(hk.hack_kv_bytes(lay, 1, s) for s in (hk.K_CODES, hk.K_META, hk.V_CODES, hk.V_META))
+    fp16 = 2 * 64 * 128 * 2
+    assert codes_meta / fp16 == 0.15625
+
+
+class _Fake:
+    """A cache struct whose pointers are non-null but never dereferenced."""
+    def __init__(self, pages=4, table=None, mbps=0):
+        c = hk.hack_kv_cache()
+        for i, n in enumerate(hk.SECTIONS):
+            setattr(c, n, 0x1000 * (i + 1))
+        c.num_pages = pages
+        if table:
+            c.block_table_dev = 0x9000
+            c.max_blocks_per_seq = mbps
+        self.struct = c
+
+
+def test_argument_errors_before_launch(lib):
+    lay = hk.hack_kv_layout_make(128, 2, 2, 32, 128)
+    L = ctypes.byref(lay)
+    fake = _Fake(pages=4)
+    C = ctypes.byref(fake.struct)
+    p = ctypes.c_void_p(0x5000)
+    # null inputs
+    assert lib.hack_quantize(L, C, None, p, p, 2, 10, None) == 1
+    # capacity: contiguous capacity is page_tokens = 128
+    assert lib.hack_quantize(L, C, p, p, p, 2, 129, None) == 3
+    assert lib.hack_append(L, C, p, p, p, 2, 128, 0, None) == 3
+    assert lib.hack_append(L, C, p, p, p, 2, 10, 5, None) == 1      # bad tail mode
+    # contiguous cache needs one page per sequence
+    assert lib.hack_quantize(L, C, p, p, p, 5, 10, None) == 1
+    # paged capacity = pages per sequence * page_tokens
+    paged = _Fake(pages=4, table=True, mbps=3)
+    assert lib.hack_quantize(L, ctypes.byref(paged.struct), p, p, p, 2, 3 * 128 + 1, None) == 3
+    # decode: workspace too small, unsupported shapes
+    ws = hk.hack_decode_workspace_bytes(lay, 2, 8, 100)
+    assert ws > 0
+    assert lib.hack_attend_decode(L, C, p, 8, p, 2, 100, 0, p, p, ws - 1, None) == 4
+    assert lib.hack_attend_decode(L, C, p, 8, p, 2, 100, 0, p, None, ws, None) == 4
+    assert lib.hack_attend_decode(L, C, p, 7, p, 2, 100, 0, p, p, ws, None) == 1      # H_q % H_kv
+    assert lib.hack_attend_decode(L, C, p, 2 * 16, p, 2, 100, 0, p, p, 10 ** 9, None) == 2   # group 16
+    lay64 = hk.hack_kv_layout_make(64, 2, 2, 32, 128)
+    assert lib.hack_attend_decode(ctypes.byref(lay64), C, p, 8, p, 2, 100, 0, p, p, 10 ** 9, None) == 2
+    lay128 = hk.hack_kv_layout_make(128, 2, 2, 128, 128)
+    assert lib.hack_attend_prefill(ctypes.byref(lay128), C, p, 8, 2, 100, 1, p, None) == 2
+    assert lib.hack_attend_prefill(L, C, p, 8, 2, 129, 1, p, None) == 3
+    # zero-sized work is a no-op that succeeds without launching
+    assert lib.hack_quantize(L, C, p, p, p, 0, 10, None) == 0
+    assert lib.hack_attend_prefill(L, C, p, 8, 2, 0, 1, p, None) == 0
+
+
+def test_workspace_grows_with_context(lib):
+    lay = hk.hack_kv_layout_make(128, 8, 2, 32, 256)
+    a = hk.hack_decode_workspace_bytes(lay, 16, 32, 4096)
+    b = hk.hack_decode_workspace_bytes(lay, 16, 32, 131072)
+    assert 0 < a <= b
+    assert hk.hack_decode_workspace_bytes(lay, 16, 31, 4096) == -1
+
+
+def test_status_strings(lib):
+    for st in range(6):
+        assert len(hk.hack_status_string(st)) > 0
+    assert hk.hack_status_string(99) == "unknown status"

@@ -301,3 +301,10 @@ def test_planted_pv_mistake_is_caught():
         return out
     assert _pv_pin_gap(wrong_count, 77, O.TAIL_REQUANT) > 1e-6
     assert _pv_pin_gap(dropped_sum_term, 77, O.TAIL_FP16) > 1e-6
+
+
+def test_empty_sequence_packs_and_attends():
+    sq = O.quantize_sequence(_f16(1, (0, 128)), _f16(2, (0, 128)), 2, 32)
+    out = O.pack_cache([[sq]], 1, 128, 2, 32, 64, 1)
+    assert not out["k_codes"].any() and not out["v_tail"].any()
+    assert np.all(O.decode_row(_f16(3, (128,)), sq) == 0)
