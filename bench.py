@@ -1,0 +1,242 @@
+"""Benchmark of the quantized-KV attention hot path on one MI355X.
+
+Default workload: Llama-3-8B-shaped decode (batch 16, 32 q heads / 8 kv heads,
+head_dim 128, context 4096, 2-bit K/V with partition 32, 4 K channels x10).
+One step = quantize-on-write of one new token per sequence (hack_append) plus
+decode attention over the whole compressed cache (hack_attend_decode).  Ten
+replicas of the cache rotate so that the 256 MB Infinity Cache cannot hold the
+working set.  Also measured: causal prefill (batch 1, 32/8 heads, 8192 tokens,
+4-bit K/V, partition 64) when the kernel is available.
+
+Prints ONE JSON line.  `value` is compressed bytes moved per step / step time.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, 8 TB/s
+INT8_PEAK_TOPS = 5000.0      # MI355X dense int8 MFMA, 5.0 POPS
+
+
+def decode_bytes_per_seq_head(L: int, d: int, bits: int, pi: int, sum_bytes: int) -> int:
+    """Compressed bytes one decode reads for one (sequence, kv head) of length L:
+    per token K codes + (min, scale) + sums; per full V block codes + (min, scale) +
+    sums for every channel; the fp16 open block."""
+    P = d // pi
+    F, T = L // pi, L % pi
+    k = L * (d * bits // 8 + P * 4 + P * sum_bytes)
+    v = F * d * (pi * bits // 8 + 4 + sum_bytes)
+    return k + v + T * d * 2
+
+
+def append_bytes(B: int, H: int, d: int, bits: int, pi: int, sum_bytes: int, T_after: int) -> int:
+    """Bytes one append moves: fp16 k/v in, one token's K partitions and the fp16
+    V value out, plus the block quantization when the open block fills."""
+    P = d // pi
+    per = 2 * d * 2 + (d * bits // 8 + P * (4 + sum_bytes)) + d * 2
+    if T_after == 0:  # the block filled: read the fp16 block, write codes + meta + sums
+        per += pi * d * 2 + d * (pi * bits // 8 + 4 + sum_bytes)
+    return B * H * per
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--replicas", type=int, default=10)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-prefill", action="store_true")
+    ap.add_argument("--prefill-iters", type=int, default=10)
+    return ap.parse_args()
+
+
+def cpu_baseline_decode(wl, budget_s: float = 15.0):
+    """The oracle timed on host cores over a bounded sample of the decode workload:
+    whole (sequence, kv head) pairs at the full context, all G query heads each."""
+    from oracle import hack_oracle as O
+    from paper_2502_03589_amd import synth
+    d, L, G = wl.head_dim, wl.context, wl.group
+    ch = synth.outlier_channels(wl.seed, d, wl.outlier_channels)
+    pairs, bytes_done, t_used = 0, 0, 0.0
+    sb = O.sum_bytes(wl.kv_bits, wl.partition)
+    while t_used < budget_s and pairs < wl.batch * wl.kv_heads:
+        b, h = divmod(pairs, wl.kv_heads)
+        k = synth.scale_channels_f16(synth.normal_f16(wl.seed, "k", (L, d), sub=1 + pairs), ch, 10.0)
+        v = synth.normal_f16(wl.seed, "v", (L, d), sub=1 + pairs)
+        q = synth.normal_f16(wl.seed, "q", (G, d), sub=1 + pairs)
+        sq = O.quantize_sequence(k, v, wl.kv_bits, wl.partition)
+        t0 = time.perf_counter()
+        for g in range(G):
+            O.decode_row(q[g], sq)
+        t_used += time.perf_counter() - t0
+        bytes_done += decode_bytes_per_seq_head(L, d, wl.kv_bits, wl.partition, sb) + G * d * (2 + 4)
+        pairs += 1
+    return {"value": round(bytes_done / t_used / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"{pairs} of {wl.batch * wl.kv_heads} (sequence, kv head) pairs at context {L}, "
+                      f"{G} query heads each; {t_used:.1f} s single-threaded numpy"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the decode path shards by "
+              f"(sequence, kv head) with no communication, so N GPUs run N independent copies.",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2502_03589_amd import hack as hk
+    from paper_2502_03589_amd import synth
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    wl = synth.WORKLOADS["decode_llama8b_l4096"]
+    B, Hq, H, d, L0 = wl.batch, wl.q_heads, wl.kv_heads, wl.head_dim, wl.context
+    bits, pi, R = wl.kv_bits, wl.partition, args.replicas
+    total_steps = args.warmup + args.steps
+    grow = (total_steps + R - 1) // R
+    cap = ((L0 + grow + pi - 1) // pi) * pi
+    lay = hk.hack_kv_layout_make(d, H, bits, pi, cap)
+
+    # inputs: K with 4 outlier channels x10, V, the new tokens and the queries
+    ch = synth.outlier_channels(wl.seed, d, wl.outlier_channels)
+    k = torch.from_numpy(synth.scale_channels_f16(synth.normal_f16(wl.seed, "k", (B, H, L0, d)), ch, 10.0)).to(dev)
+    v = torch.from_numpy(synth.normal_f16(wl.seed, "v", (B, H, L0, d))).to(dev)
+    nk = torch.from_numpy(synth.scale_channels_f16(synth.normal_f16(wl.seed, "step_k", (8, B, H, d)), ch, 10.0)).to(dev)
+    nv = torch.from_numpy(synth.normal_f16(wl.seed, "step_v", (8, B, H, d))).to(dev)
+    qs = torch.from_numpy(synth.normal_f16(wl.seed, "q", (8, B, Hq, d))).to(dev)
+    caches, lens = [], []
+    for r in range(R):
+        c = hk.KVCache(lay, B, B, None, dev)
+        ln = torch.full((B,), L0, dtype=torch.int32, device=dev)
+        if r == 0:
+            hk.hack_quantize(lay, c, k, v, ln, L0)
+        else:
+            for name in hk.SECTIONS:
+                c.buffers[name].copy_(caches[0].buffers[name])
+        caches.append(c)
+        lens.append(ln)
+    del k, v
+    ws = hk.decode_workspace(lay, B, Hq, cap)
+    out = torch.empty((B, Hq, d), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+    host_len = [L0] * R
+    sb = lay.sum_bytes
+
+    def step(i, ev=None):
+        r = i % R
+        hk.hack_append(lay, caches[r], nk[i % 8], nv[i % 8], lens[r], host_len[r], hk.TAIL_FP16, stream)
+        host_len[r] += 1
+        if ev is not None:
+            ev[0].record(stream)
+        hk.hack_attend_decode(lay, caches[r], qs[i % 8], lens[r], host_len[r], hk.TAIL_FP16, out, ws, stream)
+        if ev is not None:
+            ev[1].record(stream)
+        Lr = host_len[r]
+        dec = B * H * decode_bytes_per_seq_head(Lr, d, bits, pi, sb) + B * Hq * d * (2 + 4)
+        app = append_bytes(B, H, d, bits, pi, sb, Lr % pi)
+        return dec, app
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    dec_bytes, app_bytes = [], []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for j in range(args.steps):
+        db, ab = step(args.warmup + j, events[j])
+        dec_bytes.append(db)
+        app_bytes.append(ab)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    kern_ms = [a.elapsed_time(b) for a, b in events]
+    avg_kern_ms = float(np.mean(kern_ms))
+    step_bytes = float(np.mean(dec_bytes)) + float(np.mean(app_bytes))
+    value = step_bytes / (ms_per_step * 1e-3) / 1e9
+    achieved = float(np.mean(dec_bytes)) / (avg_kern_ms * 1e-3) / 1e9
+
+    result = {
+        "metric": "decode: compressed-KV GB/s (append + attend per step)",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int8",
+        "data": "synthetic",
+        "config": {"workload": "decode_llama8b_l4096", "batch": B, "q_heads": Hq, "kv_heads": H,
+                   "head_dim": d, "context": L0, "kv_bits": bits, "partition": pi, "qp_bits": 8,
+                   "outlier_k_channels": wl.outlier_channels, "cache_replicas": R,
+                   "step": "append 1 token + decode attention", "parallelism": "1 GPU"},
+        "roofline": {"bound": "hbm", "kernel": "decode_kernel", "achieved": round(achieved, 2),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": None, "avg_kernel_us": round(avg_kern_ms * 1e3, 3),
+                     "bytes_per_launch": int(np.mean(dec_bytes))},
+    }
+    if not args.no_prefill:
+        result["prefill"] = bench_prefill(args.prefill_iters)
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline_decode(wl)
+    print(json.dumps(result), flush=True)
+
+
+def bench_prefill(iters: int):
+    """Causal prefill (batch 1, 32/8 heads, 8192 tokens, 4-bit K/V, partition 64):
+    quantize-on-write of the prompt's K/V then attention; int8 ops of the causal
+    triangle = 2 products x 32 heads x L(L+1)/2 x 128 x 2."""
+    import torch
+    from paper_2502_03589_amd import hack as hk
+    from paper_2502_03589_amd import synth
+    wl = synth.WORKLOADS["prefill_l8192"]
+    B, Hq, H, d, L = wl.batch, wl.q_heads, wl.kv_heads, wl.head_dim, wl.context
+    dev = torch.device("cuda:0")
+    lay = hk.hack_kv_layout_make(d, H, wl.kv_bits, wl.partition, L)
+    c = hk.KVCache(lay, B, B, None, dev)
+    k = torch.from_numpy(synth.normal_f16(wl.seed, "k", (B, H, L, d))).to(dev)
+    v = torch.from_numpy(synth.normal_f16(wl.seed, "v", (B, H, L, d))).to(dev)
+    q = torch.from_numpy(synth.normal_f16(wl.seed, "q", (B, Hq, L, d))).to(dev)
+    ln = torch.full((B,), L, dtype=torch.int32, device=dev)
+    out = torch.empty((B, Hq, L, d), dtype=torch.float32, device=dev)
+    hk.hack_quantize(lay, c, k, v, ln, L)
+    try:
+        hk.hack_attend_prefill(lay, c, q, True, out)
+    except hk.HackError as e:
+        return {"status": f"unavailable: {e}"}
+    torch.cuda.synchronize()
+    ops = 2 * Hq * (L * (L + 1) // 2) * d * 2 * B
+    e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+    qt, at = [], []
+    for _ in range(iters):
+        e0.record()
+        hk.hack_quantize(lay, c, k, v, ln, L)
+        e1.record()
+        hk.hack_attend_prefill(lay, c, q, True, out)
+        e2.record()
+        torch.cuda.synchronize()
+        qt.append(e0.elapsed_time(e1))
+        at.append(e1.elapsed_time(e2))
+    a_ms = float(np.median(at))
+    tops = ops / (a_ms * 1e-3) / 1e12
+    return {"workload": "prefill_l8192", "int8_ops": ops, "attend_ms": round(a_ms, 4),
+            "quantize_ms": round(float(np.median(qt)), 4), "TOPS": round(tops, 2),
+            "peak_TOPS": INT8_PEAK_TOPS, "frac": round(tops / INT8_PEAK_TOPS, 4)}
+
+
+if __name__ == "__main__":
+    main()

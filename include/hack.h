@@ -146,8 +146,9 @@ hack_status hack_append(const hack_kv_layout* layout, const hack_kv_cache* cache
                         const void* k_new_dev, const void* v_new_dev, int32_t* seq_lens_dev,
                         int32_t batch, int32_t max_len, int32_t tail_mode, hipStream_t stream);
 
-/* Workspace bytes hack_attend_decode needs for these sizes (split-K partial results
- * and per-(sequence, kv head) arrival counters).  -1 on invalid arguments. */
+/* Workspace bytes hack_attend_decode needs for these sizes (the split-K partial
+ * results: max, sum and unnormalized O per chunk and query head).  -1 on invalid
+ * arguments. */
 int64_t hack_decode_workspace_bytes(const hack_kv_layout* layout, int32_t batch,
                                     int32_t num_q_heads, int32_t max_len);
 
@@ -156,9 +157,10 @@ int64_t hack_decode_workspace_bytes(const hack_kv_layout* layout, int32_t batch,
  * attends kv head h / (H_q/H_kv).  Per sequence, all seq_lens[s] cached tokens are
  * attended (0 <= seq_lens[s] <= max_len; a sequence of length 0 yields zeros).
  * out_dev: fp32 [batch][H_q][head_dim].  workspace_dev must hold
- * hack_decode_workspace_bytes(...) bytes, be zero-filled before its first use, and
- * not be shared by calls that may run concurrently; every call leaves it reusable.
- * Requires head_dim 128, partition 32, 64 or 128, and H_q/H_kv <= 16 (else
+ * hack_decode_workspace_bytes(...) bytes (no initialization needed) and must not
+ * be shared by calls that may run concurrently.  One or two kernels are launched
+ * (the second merges the chunks of long sequences).
+ * Requires head_dim 128, partition 32 or 64, and H_q/H_kv <= 8 (else
  * HACK_ERR_UNSUPPORTED). */
 hack_status hack_attend_decode(const hack_kv_layout* layout, const hack_kv_cache* cache,
                                const void* q_dev, int32_t num_q_heads, const int32_t* seq_lens_dev,
@@ -170,8 +172,8 @@ hack_status hack_attend_decode(const hack_kv_layout* layout, const hack_kv_cache
  * hack_quantize with all seq_lens = len.  q_dev: fp16 [batch][H_q][len][head_dim];
  * out_dev: fp32 [batch][H_q][len][head_dim].  causal != 0 masks token j > i for
  * query i; the masked zeros of P inside a block are quantized with the block.  The
- * open V block is used in fp16.  Requires head_dim 128, partition 32, 64 or 128,
- * H_q % H_kv == 0 and H_q/H_kv <= 16 (else HACK_ERR_UNSUPPORTED). */
+ * open V block is used in fp16.  Requires head_dim 128, partition 32 or 64,
+ * H_q % H_kv == 0 and H_q/H_kv <= 8 (else HACK_ERR_UNSUPPORTED). */
 hack_status hack_attend_prefill(const hack_kv_layout* layout, const hack_kv_cache* cache,
                                 const void* q_dev, int32_t num_q_heads, int32_t batch, int32_t len,
                                 int32_t causal, float* out_dev, hipStream_t stream);

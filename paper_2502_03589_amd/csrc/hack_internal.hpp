@@ -16,8 +16,7 @@ namespace hack {
 struct DecodePlan {
   int chunk;
   int splits;
-  int64_t partial_floats;   // batch * H_kv * splits * G * (2 + head_dim)
-  int64_t counter_offset;   // byte offset of the int32 counters in the workspace
+  int64_t partial_floats;   // batch * H_kv * splits * G * (4 + head_dim)
   int64_t workspace_bytes;
 };
 
@@ -38,8 +37,7 @@ struct DecodeArgs {
   const __half* q;        // [B][H_q][128]
   const int32_t* lens;    // [B]
   float* out;             // [B][H_q][128]
-  float* partials;        // [B][H_kv][splits][G][2 + 128]
-  int32_t* counters;      // [B][H_kv]
+  float* partials;        // [B][H_kv][splits][G][4 + 128]: max, sum, pad, O
   int num_q_heads;
   int group;              // H_q / H_kv
   int chunk;
