@@ -1,12 +1,496 @@
 // Prefill attention on quantized Q/K/V/P (Sec. 5.3 with L_Q = L_KV; Eq. 2-4).
+//
+// One workgroup of eight 64-lane wavefronts per (32 query rows, up to 4 query heads
+// of one kv group, sequence); wave w owns query head 4*hg + (w % 4) of the group and
+// the 16 rows r0 + 16*(w / 4) ...  The workgroup walks the V blocks (PI tokens each)
+// up to the causal diagonal:
+//   staging  the 512 threads load block kb+1 (K codes unpacked to int8 in channel
+//            order, V codes unpacked to int8 in the token order of the P.V operand,
+//            per-token K and per-channel V metadata) into the other LDS buffer while
+//            the waves compute block kb.
+//   S^T = K'Q'^T  v_mfma_i32_16x16{32,64}_i8, one per (16-token tile, 16-row tile,
+//            K partition): A = K codes (lane = token), B = 8-bit Q codes minus 128
+//            quantized in registers (lane = query row).  Lane (row n, group g) gets
+//            tokens 4g..4g+3 of the tile for row n; Eq. 4 with cached K sums on VALU.
+//   softmax  online per row with a lazily raised reference max; causal mask.
+//   P        8-bit per (row, V block) with round-to-nearest-even codes; the masked
+//            zeros inside the diagonal block are quantized with it.  The lane's codes
+//            are already the B operand of the P.V product (no transpose).
+//   O^T = V'^T P'^T  one MFMA per (16-channel tile, row tile); an all-ones A gives
+//            the P code sums; Eq. 4 with the cached V sums on the VALU.
+//   open block  (len mod PI tokens) multiplied in fp16 with unquantized p.
 #include "hack_internal.hpp"
 
 namespace hack {
 
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+namespace {
+
+constexpr int kRows = 32;        // query rows per workgroup (two 16-row MFMA tiles)
+constexpr float kScale = 0.12751743074941640f;  // log2(e) / sqrt(128)
+constexpr float kSlack = 8.0f;   // reference max raised only beyond this (log2 units)
+
+template <int PI>
+struct PrefillCfg {
+  static constexpr int D = 128;
+  static constexpr int P = D / PI;    // K partitions per token
+  static constexpr int TL = PI / 16;  // 16-token tiles per block
+  static constexpr int KSL = PI / 4;  // operand bytes per lane per MFMA (k-slots of a lane group)
+  static constexpr int KROW = D + 16; // LDS row stride of unpacked K (bytes)
+  static constexpr int VROW = PI + 16;// LDS row stride of unpacked V (bytes)
+};
+
+// int8 MFMA with K = PI: 16x16x64 (16 bytes per lane) or 16x16x32 (8 bytes per lane).
+template <int PI>
+struct Op;
+template <>
+struct Op<64> {
+  typedef v4i T;
+  static __device__ __forceinline__ v4i mfma(v4i a, v4i b, v4i c) {
+    return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
+  }
+  static __device__ __forceinline__ v4i lds(const int8_t* p) {
+    const int4 w = *reinterpret_cast<const int4*>(p);
+    return v4i{w.x, w.y, w.z, w.w};
+  }
+  static __device__ __forceinline__ v4i ones() { return v4i{0x01010101, 0x01010101, 0x01010101, 0x01010101}; }
+  static __device__ __forceinline__ v4i from(const uint32_t* w) {
+    return v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
+  }
+};
+template <>
+struct Op<32> {
+  typedef long T;
+  static __device__ __forceinline__ v4i mfma(long a, long b, v4i c) {
+    return __builtin_amdgcn_mfma_i32_16x16x32_i8(a, b, c, 0, 0, 0);
+  }
+  static __device__ __forceinline__ long lds(const int8_t* p) { return *reinterpret_cast<const long*>(p); }
+  static __device__ __forceinline__ long ones() { return 0x0101010101010101L; }
+  static __device__ __forceinline__ long from(const uint32_t* w) {
+    return (long)(((uint64_t)w[1] << 32) | (uint64_t)w[0]);
+  }
+};
+
+// LDS of one staged V block.
+template <int PI>
+struct Stage {
+  int8_t k[PI][PrefillCfg<PI>::KROW];          // K codes, [token][channel]
+  int8_t v[128][PrefillCfg<PI>::VROW];         // V codes, [channel][operand position]
+  float km[PrefillCfg<PI>::P][3][PI];          // per token and partition: s_k, s_k*sum k', m_k
+  float vm[3][128];                            // per channel: s_v, m_v, s_v*sum v' + PI*m_v
+};
+
+// Max / min / sum over the four lane groups (lanes l, l^16, l^32, l^48).
+__device__ __forceinline__ float xg_max(float x) {
+  auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float xg_min(float x) {
+  auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fminf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fminf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float xg_sum(float x) {
+  auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+__device__ __forceinline__ int xg_sum_i(int x) {
+  auto a = __builtin_amdgcn_permlane32_swap((uint32_t)x, (uint32_t)x, false, false);
+  x = (int)a[0] + (int)a[1];
+  auto b = __builtin_amdgcn_permlane16_swap((uint32_t)x, (uint32_t)x, false, false);
+  return (int)b[0] + (int)b[1];
+}
+
+struct PrefillArgs {
+  CacheView c;
+  const __half* q;   // [B][H_q][L][128]
+  float* out;        // [B][H_q][L][128]
+  int num_q_heads;
+  int group;
+  int head_groups;   // ceil(group / 4)
+  int len;
+  int causal;
+  int nqb;           // query blocks of kRows rows
+};
+
+// Staging of one V block by the 512 threads of the workgroup (threads 0-255: K,
+// threads 256-511: V), in two phases so that the global loads of block kb+1 are in
+// flight while block kb is computed: stage_load() fills registers, stage_store()
+// unpacks them into LDS.
+template <int BITS, int PI>
+struct StageRegs {
+  static constexpr int KW = (PI / 2) * BITS / 32;  // K code dwords per thread
+  uint32_t w[KW];     // K codes (threads 0-255) or V codes (threads 256-511)
+  uint32_t meta, sum; // K metadata of (token, partition) or V metadata of a channel
+};
+
+template <int BITS, int PI>
+__device__ __forceinline__ void stage_load(const PrefillArgs& a, StageRegs<BITS, PI>& r, int s, int hkv, int kb,
+                                           bool with_v) {
+  constexpr int D = 128, P = PrefillCfg<PI>::P;
+  constexpr int CPT = PI / 2, TPR = D / CPT;
+  const CacheView& c = a.c;
+  const int tid = threadIdx.x;
+  const int64_t page = page_of(c, s, kb * PI);
+  const int64_t krow0 = (page * c.kv_heads + hkv) * c.page_tokens + (int64_t)(kb * PI) % c.page_tokens;
+  r.meta = 0u;
+  r.sum = 0u;
+#pragma unroll
+  for (int i = 0; i < StageRegs<BITS, PI>::KW; ++i) r.w[i] = 0u;
+  if (tid < 256) {
+    // K codes: thread -> (token tid / TPR, PI/2 channels)
+    const int tt = tid / TPR, cb = (tid % TPR) * CPT;
+    const uint32_t* src = reinterpret_cast<const uint32_t*>(c.k_codes + (krow0 + tt) * (D * BITS / 8) + cb * BITS / 8);
+#pragma unroll
+    for (int i = 0; i < StageRegs<BITS, PI>::KW; ++i) r.w[i] = src[i];
+    if (tid < PI * P) {  // K metadata: thread -> (token, partition)
+      const int64_t mi = (krow0 + tid / P) * P + tid % P;
+      r.meta = reinterpret_cast<const uint32_t*>(c.k_meta)[mi];
+      r.sum = load_sum(c.k_sums, mi, c.sum_bytes);
+    }
+  } else if (with_v) {
+    const int64_t vb = (page * c.kv_heads + hkv) * (c.page_tokens / PI) + ((int64_t)(kb * PI) % c.page_tokens) / PI;
+    const int vt = tid - 256;
+    // V codes: two threads per channel, PI/2 tokens each
+    const int ch = vt >> 1, half = vt & 1;
+    const uint32_t* src = reinterpret_cast<const uint32_t*>(c.v_codes + (vb * D + ch) * (PI * BITS / 8) +
+                                                            half * (PI / 2) * BITS / 8);
+#pragma unroll
+    for (int i = 0; i < StageRegs<BITS, PI>::KW; ++i) r.w[i] = src[i];
+    if (vt < D) {
+      r.meta = reinterpret_cast<const uint32_t*>(c.v_meta)[vb * D + vt];
+      r.sum = load_sum(c.v_sums, vb * D + vt, c.sum_bytes);
+    }
+  }
+}
+
+template <int BITS, int PI>
+__device__ __forceinline__ void stage_store(const StageRegs<BITS, PI>& r, Stage<PI>& st, bool with_v) {
+  using C = PrefillCfg<PI>;
+  constexpr int D = 128, P = C::P, KSL = C::KSL;
+  constexpr int CPT = PI / 2, TPR = D / CPT;
+  const int tid = threadIdx.x;
+  if (tid < 256) {
+    // K codes unpacked to int8 in channel order
+    const int tt = tid / TPR, cb = (tid % TPR) * CPT;
+    uint32_t* dst = reinterpret_cast<uint32_t*>(&st.k[tt][cb]);
+#pragma unroll
+    for (int e4 = 0; e4 < CPT / 4; ++e4) {
+      uint32_t v = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int e = 4 * e4 + i;
+        v |= ((r.w[(e * BITS) / 32] >> ((e * BITS) % 32)) & ((1u << BITS) - 1)) << (8 * i);
+      }
+      dst[e4] = v;
+    }
+    if (tid < PI * P) {
+      const int tt2 = tid / P, p = tid % P;
+      const float mk = __half2float(__ushort_as_half((uint16_t)(r.meta & 0xFFFFu)));
+      const float sk = __half2float(__ushort_as_half((uint16_t)(r.meta >> 16)));
+      st.km[p][0][tt2] = sk;
+      st.km[p][1][tt2] = sk * (float)r.sum;
+      st.km[p][2][tt2] = mk;
+    }
+  } else if (with_v) {
+    // V codes: token tau = 16*tl + 4*g + i goes to operand position g*KSL + 4*tl + i
+    const int vt = tid - 256;
+    const int ch = vt >> 1, half = vt & 1;
+#pragma unroll
+    for (int q4 = 0; q4 < PI / 8; ++q4) {
+      uint32_t v = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int e = 4 * q4 + i;
+        v |= ((r.w[(e * BITS) / 32] >> ((e * BITS) % 32)) & ((1u << BITS) - 1)) << (8 * i);
+      }
+      const int tau0 = half * (PI / 2) + 4 * q4;
+      const int tl = tau0 >> 4, g = (tau0 >> 2) & 3;
+      *reinterpret_cast<uint32_t*>(&st.v[ch][g * KSL + 4 * tl]) = v;
+    }
+    if (vt < D) {
+      const float mv = __half2float(__ushort_as_half((uint16_t)(r.meta & 0xFFFFu)));
+      const float sv = __half2float(__ushort_as_half((uint16_t)(r.meta >> 16)));
+      st.vm[0][vt] = sv;
+      st.vm[1][vt] = mv;
+      st.vm[2][vt] = fmaf((float)PI, mv, sv * (float)r.sum);
+    }
+  }
+}
+
+}  // namespace
+
+template <int BITS, int PI>
+__global__ __launch_bounds__(512, 1) void prefill_kernel(PrefillArgs a) {
+  using C = PrefillCfg<PI>;
+  using OP = Op<PI>;
+  typedef typename OP::T opT;
+  constexpr int D = 128, P = C::P, TL = C::TL, KSL = C::KSL;
+
+  __shared__ __attribute__((aligned(16))) Stage<PI> stages[2];
+  __shared__ float ptail[8][16][PI];
+
+  const CacheView& c = a.c;
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+  const int col = lane & 15, grp = lane >> 4;
+  const int s = blockIdx.z;
+  const int hkv = blockIdx.y / a.head_groups, hg = blockIdx.y % a.head_groups;
+  const int qb = a.causal ? (a.nqb - 1 - (int)blockIdx.x) : (int)blockIdx.x;  // heavy blocks first
+  const int r0 = qb * kRows;
+  const int L = a.len;
+  const int gh = 4 * hg + (wave & 3);
+  const bool head_ok = gh < a.group;
+  const int hq = hkv * a.group + (head_ok ? gh : 0);
+  const int row = r0 + 16 * (wave >> 2) + col;  // this lane's query row
+  const int F = L / PI, T = L - F * PI;
+  const int nblk_q = F + (T > 0 ? 1 : 0);
+  const int nblk = a.causal ? min(nblk_q, (min(r0 + kRows, L) - 1) / PI + 1) : nblk_q;
+
+  // ---- Q row: 8-bit codes per partition (float32 metadata), in MFMA operand layout ----
+  opT qop[P];
+  float sq[P], mq[P], rq[P];
+  {
+    const bool rv = head_ok && row < L;
+    const __half* qrow = a.q + (((int64_t)s * a.num_q_heads + hq) * L + (rv ? row : 0)) * D;
+#pragma unroll
+    for (int p = 0; p < P; ++p) {
+      float x[KSL];
+      const int c0 = p * PI + grp * KSL;
+#pragma unroll
+      for (int e = 0; e < KSL; e += 2) {
+        const float2 f = rv ? __half22float2(*reinterpret_cast<const __half2*>(qrow + c0 + e)) : float2{0.0f, 0.0f};
+        x[e] = f.x;
+        x[e + 1] = f.y;
+      }
+      float mn = x[0], mx = x[0];
+#pragma unroll
+      for (int e = 1; e < KSL; ++e) {
+        mn = fminf(mn, x[e]);
+        mx = fmaxf(mx, x[e]);
+      }
+      mn = xg_min(mn);
+      mx = xg_max(mx);
+      uint32_t w[KSL / 4];
+      int csum = 0;
+      float s32;
+      {
+#pragma clang fp contract(off)
+        s32 = __fdiv_rn(__fsub_rn(mx, mn), 255.0f);
+        const float r = s32 != 0.0f ? __fdiv_rn(1.0f, s32) : 0.0f;
+#pragma unroll
+        for (int e4 = 0; e4 < KSL / 4; ++e4) {
+          uint32_t v = 0;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float t = __fmul_rn(__fsub_rn(x[4 * e4 + i], mn), r);
+            const int code = s32 != 0.0f ? (int)fminf(rintf(t), 255.0f) : 0;
+            csum += code;
+            v |= (uint32_t)(code ^ 0x80) << (8 * i);
+          }
+          w[e4] = v;
+        }
+      }
+      csum = xg_sum_i(csum);
+      qop[p] = OP::from(w);
+      // Eq. 4 coefficients in log2 units: s_q, m~_q = m_q + 128 s_q, R = s_q sum q' + n m_q
+      sq[p] = kScale * s32;
+      mq[p] = kScale * (mn + 128.0f * s32);
+      rq[p] = kScale * (s32 * (float)csum + (float)PI * mn);
+    }
+  }
+
+  float m_ref = -INFINITY, l_run = 0.0f;
+  float o[8][4];
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) o[j][i] = 0.0f;
+
+  StageRegs<BITS, PI> sr;
+  if (nblk > 0) {
+    stage_load<BITS, PI>(a, sr, s, hkv, 0, 0 < F);
+    stage_store<BITS, PI>(sr, stages[0], 0 < F);
+  }
+  __syncthreads();
+
+  for (int kb = 0; kb < nblk; ++kb) {
+    Stage<PI>& st = stages[kb & 1];
+    const bool next = kb + 1 < nblk;
+    if (next) stage_load<BITS, PI>(a, sr, s, hkv, kb + 1, kb + 1 < F);
+    const bool is_tail = kb >= F;  // the fp16 open block
+    const int tb0 = kb * PI;
+
+    // ---------------- S^T tiles and Eq. 4 (lane: row `row`, tokens 16 tl + 4 grp + i) ----------------
+    float sv[TL][4];
+#pragma unroll
+    for (int tl = 0; tl < TL; ++tl) {
+      float acc_s[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int p = 0; p < P; ++p) {
+        const opT ka = OP::lds(&st.k[16 * tl + col][p * PI + grp * KSL]);
+        const v4i acc = OP::mfma(ka, qop[p], v4i{0, 0, 0, 0});
+        const float4 f0 = *reinterpret_cast<const float4*>(&st.km[p][0][16 * tl + 4 * grp]);
+        const float4 f1 = *reinterpret_cast<const float4*>(&st.km[p][1][16 * tl + 4 * grp]);
+        const float4 f2 = *reinterpret_cast<const float4*>(&st.km[p][2][16 * tl + 4 * grp]);
+        const float ksk[4] = {f0.x, f0.y, f0.z, f0.w};
+        const float kak[4] = {f1.x, f1.y, f1.z, f1.w};
+        const float kmk[4] = {f2.x, f2.y, f2.z, f2.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          // s_q s_k C~ + m~_q (s_k sum k') + R m_k
+          float x = fmaf(sq[p] * ksk[i], (float)acc[i], acc_s[i]);
+          x = fmaf(mq[p], kak[i], x);
+          acc_s[i] = fmaf(rq[p], kmk[i], x);
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int tok = tb0 + 16 * tl + 4 * grp + i;
+        const bool masked = tok >= L || (a.causal && tok > row);
+        sv[tl][i] = masked ? -INFINITY : acc_s[i];
+      }
+    }
+
+    // ---------------- softmax and P codes ----------------
+    float bmax = -INFINITY;
+#pragma unroll
+    for (int tl = 0; tl < TL; ++tl)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) bmax = fmaxf(bmax, sv[tl][i]);
+    bmax = xg_max(bmax);
+    if (bmax > m_ref + kSlack || (m_ref == -INFINITY && bmax > -INFINITY)) {  // raise the reference max
+      const float alpha = __builtin_amdgcn_exp2f(m_ref - bmax);
+      l_run *= alpha;
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[j][i] *= alpha;
+      m_ref = bmax;
+    }
+    float pt[TL][4];
+    float pmin = INFINITY, lsum = 0.0f;
+#pragma unroll
+    for (int tl = 0; tl < TL; ++tl)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        pt[tl][i] = __builtin_amdgcn_exp2f(sv[tl][i] - m_ref);  // masked: exp2(-inf) = 0
+        lsum += pt[tl][i];
+        pmin = fminf(pmin, pt[tl][i]);
+      }
+    l_run += lsum;
+
+    if (!is_tail) {
+      pmin = xg_min(pmin);
+      const float pmax = bmax > -INFINITY ? __builtin_amdgcn_exp2f(bmax - m_ref) : 0.0f;
+      const float dp = pmax - pmin;
+      const float r = dp > 0.0f ? 255.0f * __builtin_amdgcn_rcpf(dp) : 0.0f;
+      const float bias = -pmin * r;
+      uint32_t w[TL];
+#pragma unroll
+      for (int tl = 0; tl < TL; ++tl) {
+        uint32_t v = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v = __builtin_amdgcn_cvt_pk_u8_f32(fmaf(pt[tl][i], r, bias), i, v);
+        w[tl] = v ^ 0x80808080u;  // codes - 128
+      }
+      const opT pop = OP::from(w);
+      const float ps = dp * (1.0f / 255.0f);   // s_p
+      const float pm = pmin + 128.0f * ps;     // m~_p
+      // sum of the signed codes of this row's block: all-ones A operand
+      const v4i z = OP::mfma(OP::ones(), pop, v4i{0, 0, 0, 0});
+      const float pz = ps * (float)z[0];       // s_p * sum p~'
+
+      // ---------------- O^T += V'^T P'^T with Eq. 4 (lane: row, channels 16 j + 4 grp + i) ----------------
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const opT va = OP::lds(&st.v[16 * j + col][grp * KSL]);
+        const v4i acc = OP::mfma(va, pop, v4i{0, 0, 0, 0});
+        const float4 fs = *reinterpret_cast<const float4*>(&st.vm[0][16 * j + 4 * grp]);
+        const float4 fm = *reinterpret_cast<const float4*>(&st.vm[1][16 * j + 4 * grp]);
+        const float4 fb = *reinterpret_cast<const float4*>(&st.vm[2][16 * j + 4 * grp]);
+        const float vs[4] = {fs.x, fs.y, fs.z, fs.w};
+        const float vmn[4] = {fm.x, fm.y, fm.z, fm.w};
+        const float vbar[4] = {fb.x, fb.y, fb.z, fb.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          // s_p s_v D~ + (s_p sum p~') m_v + m~_p (s_v sum v' + n m_v)
+          float x = fmaf(ps * vs[i], (float)acc[i], o[j][i]);
+          x = fmaf(pz, vmn[i], x);
+          o[j][i] = fmaf(pm, vbar[i], x);
+        }
+      }
+    } else {
+      // fp16 open block: O[row][ch] += sum_{t < T} p[row][t] v_t[ch] with unquantized p
+#pragma unroll
+      for (int tl = 0; tl < TL; ++tl)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) ptail[wave][col][16 * tl + 4 * grp + i] = pt[tl][i];
+      __builtin_amdgcn_s_waitcnt(0xC07F);
+      __builtin_amdgcn_wave_barrier();
+      const __half* vt = c.v_tail + (((int64_t)s * c.kv_heads + hkv) * PI) * D;
+      for (int t = 0; t < T; ++t) {
+        const float pr = ptail[wave][col][t];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const uint2 raw = *reinterpret_cast<const uint2*>(vt + (int64_t)t * D + 16 * j + 4 * grp);
+          const float2 v01 = __half22float2(*reinterpret_cast<const __half2*>(&raw.x));
+          const float2 v23 = __half22float2(*reinterpret_cast<const __half2*>(&raw.y));
+          o[j][0] = fmaf(pr, v01.x, o[j][0]);
+          o[j][1] = fmaf(pr, v01.y, o[j][1]);
+          o[j][2] = fmaf(pr, v23.x, o[j][2]);
+          o[j][3] = fmaf(pr, v23.y, o[j][3]);
+        }
+      }
+    }
+    if (next) stage_store<BITS, PI>(sr, stages[(kb + 1) & 1], kb + 1 < F);
+    __syncthreads();  // stage kb+1 complete; stage kb free for kb+2
+  }
+
+  // ---- normalize and write O[row][16 j + 4 grp + i] ----
+  const float lsum = xg_sum(l_run);
+  if (head_ok && row < L) {
+    const float inv = lsum > 0.0f ? 1.0f / lsum : 0.0f;
+    float* dst = a.out + (((int64_t)s * a.num_q_heads + hq) * L + row) * D;
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      *reinterpret_cast<float4*>(dst + 16 * j + 4 * grp) =
+          float4{o[j][0] * inv, o[j][1] * inv, o[j][2] * inv, o[j][3] * inv};
+  }
+}
+
+template <int BITS, int PI>
+static hipError_t prefill_impl(const PrefillArgs& a, int batch, hipStream_t stream) {
+  dim3 grid((unsigned)a.nqb, (unsigned)(a.c.kv_heads * a.head_groups), (unsigned)batch);
+  hipLaunchKernelGGL((prefill_kernel<BITS, PI>), grid, dim3(512), 0, stream, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_prefill(const hack_kv_layout& lay, const CacheView& c, const __half* q, int num_q_heads,
                           int batch, int len, int causal, float* out, hipStream_t stream) {
-  (void)lay; (void)c; (void)q; (void)num_q_heads; (void)batch; (void)len; (void)causal; (void)out; (void)stream;
-  return hipErrorNotSupported;
+  PrefillArgs a;
+  a.c = c;
+  a.q = q;
+  a.out = out;
+  a.num_q_heads = num_q_heads;
+  a.group = num_q_heads / lay.num_kv_heads;
+  a.head_groups = (a.group + 3) / 4;
+  a.len = len;
+  a.causal = causal;
+  a.nqb = (len + kRows - 1) / kRows;
+  switch (lay.kv_bits * 1000 + lay.partition) {
+    case 2032: return prefill_impl<2, 32>(a, batch, stream);
+    case 2064: return prefill_impl<2, 64>(a, batch, stream);
+    case 4032: return prefill_impl<4, 32>(a, batch, stream);
+    case 4064: return prefill_impl<4, 64>(a, batch, stream);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 }  // namespace hack
