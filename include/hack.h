@@ -141,7 +141,7 @@ hack_status hack_quantize(const hack_kv_layout* layout, const hack_kv_cache* cac
  * attended with the tail mode it was appended with.  seq_lens_dev is incremented on
  * the device.  max_len is a host upper bound of seq_lens before the call; returns
  * HACK_ERR_CAPACITY if max_len + 1 exceeds the capacity (the kernel also skips any
- * sequence already at capacity). */
+ * sequence already at capacity); HACK_ERR_UNSUPPORTED if H_kv * head_dim > 2048. */
 hack_status hack_append(const hack_kv_layout* layout, const hack_kv_cache* cache,
                         const void* k_new_dev, const void* v_new_dev, int32_t* seq_lens_dev,
                         int32_t batch, int32_t max_len, int32_t tail_mode, hipStream_t stream);

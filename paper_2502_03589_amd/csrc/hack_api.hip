@@ -132,6 +132,7 @@ hack_status hack_append(const hack_kv_layout* layout, const hack_kv_cache* cache
   const int64_t cap = cache_capacity(layout, cache, batch);
   if (cap < 0) return HACK_ERR_INVALID_ARGUMENT;
   if ((int64_t)max_len + 1 > cap) return HACK_ERR_CAPACITY;
+  if (layout->num_kv_heads * layout->head_dim > 2048) return HACK_ERR_UNSUPPORTED;  // one workgroup per sequence
   if (batch == 0) return HACK_OK;
   (void)hipGetLastError();
   return from_hip(hack::launch_append(*layout, make_view(layout, cache), static_cast<const __half*>(k_new_dev),

@@ -98,54 +98,69 @@ __global__ __launch_bounds__(256) void quantize_v_kernel(CacheView c, const __ha
 
 // One new token per sequence: K partitions of the token; V value into the fp16
 // open block, which is quantized when it fills (and on every call in REQUANT mode).
+// The new token's values are loaded together with the sequence length (they do not
+// depend on it) so that the kernel pays one memory round trip before its stores.
 template <int BITS, int PI>
 __global__ __launch_bounds__(256) void append_kernel(CacheView c, const __half* __restrict__ k_new,
                                                      const __half* __restrict__ v_new, int32_t* lens,
                                                      int capacity, int requant, int stochastic,
                                                      uint64_t key_k, uint64_t key_v) {
-  __shared__ int s_len;
+  constexpr int MAXV = 8;  // V channels per thread: H * d <= 256 * MAXV
   const int s = blockIdx.x;
-  if (threadIdx.x == 0) s_len = lens[s];
-  __syncthreads();
-  const int L = s_len;
-  if (L < 0 || L >= capacity) return;  // uniform across the workgroup
   const int H = c.kv_heads, d = c.head_dim, P = d / PI;
-  for (int w = threadIdx.x; w < H * P; w += blockDim.x) {
-    const int h = w / P, p = w % P;
-    float x[PI];
-    load_f16_run<PI>(k_new + ((int64_t)s * H + h) * d + p * PI, x);
+  const int nk = H * P, nv = H * d;
+  // K partition of this thread (one per thread for H * P <= 256)
+  float xk[PI];
+  const bool has_k = (int)threadIdx.x < nk;
+  if (has_k) {
+    const int h = threadIdx.x / P, p = threadIdx.x % P;
+    load_f16_run<PI>(k_new + ((int64_t)s * H + h) * d + p * PI, xk);
+  }
+  __half vn[MAXV];
+#pragma unroll
+  for (int i = 0; i < MAXV; ++i) {
+    const int w = threadIdx.x + i * blockDim.x;
+    vn[i] = w < nv ? v_new[(int64_t)s * nv + w] : __float2half(0.0f);
+  }
+  const int L = lens[s];
+  if (L < 0 || L >= capacity) return;  // uniform across the workgroup
+  if (has_k) {
+    const int h = threadIdx.x / P, p = threadIdx.x % P;
     uint32_t words[(PI * BITS + 31) / 32];
     uint16_t mb, sb;
     const uint32_t sum = quantize_values<BITS, PI>(
-        x, PI, stochastic != 0, key_k, element_index(s, H, h, L, d, p * PI), 1ull, words, mb, sb);
+        xk, PI, stochastic != 0, key_k, element_index(s, H, h, L, d, p * PI), 1ull, words, mb, sb);
     const int64_t row = k_row(c, s, h, L);
     store_codes<BITS, PI>(c.k_codes + row * (d * BITS / 8) + p * (PI * BITS / 8), words);
     reinterpret_cast<uint32_t*>(c.k_meta)[row * P + p] = (uint32_t)mb | ((uint32_t)sb << 16);
     store_sum(c.k_sums, row * P + p, c.sum_bytes, sum);
   }
   const int F = L / PI, T = L - F * PI;  // the new token is element T of block F
-  for (int w = threadIdx.x; w < H * d; w += blockDim.x) {
+  const bool quantize_v = T + 1 == PI || requant;
+#pragma unroll
+  for (int i = 0; i < MAXV; ++i) {
+    const int w = threadIdx.x + i * blockDim.x;
+    if (w >= nv) break;
     const int h = w / d, ch = w % d;
-    const __half vn = v_new[((int64_t)s * H + h) * d + ch];
     __half* tail = c.v_tail + (((int64_t)s * H + h) * PI) * d + ch;
-    tail[(int64_t)T * d] = vn;
-    const int n = T + 1;
-    if (n == PI || requant) {
+    tail[(int64_t)T * d] = vn[i];
+    if (quantize_v) {
+      const int n = T + 1;
       float x[PI];
 #pragma unroll
       for (int e = 0; e < PI; ++e)
-        x[e] = e < T ? __half2float(tail[(int64_t)e * d]) : (e == T ? __half2float(vn) : 0.0f);
+        x[e] = e < T ? __half2float(tail[(int64_t)e * d]) : (e == T ? __half2float(vn[i]) : 0.0f);
       uint32_t words[(PI * BITS + 31) / 32];
       uint16_t mb, sb;
       const uint32_t sum = quantize_values<BITS, PI>(
           x, n, stochastic != 0, key_v, element_index(s, H, h, F * PI, d, ch), (uint64_t)d, words, mb, sb);
-      const int64_t vb = v_block<PI>(c, s, h, F * PI);
-      store_codes<BITS, PI>(c.v_codes + (vb * d + ch) * (PI * BITS / 8), words);
-      reinterpret_cast<uint32_t*>(c.v_meta)[vb * d + ch] = (uint32_t)mb | ((uint32_t)sb << 16);
-      store_sum(c.v_sums, vb * d + ch, c.sum_bytes, sum);
+      const int64_t vbh = v_block<PI>(c, s, h, F * PI);
+      store_codes<BITS, PI>(c.v_codes + (vbh * d + ch) * (PI * BITS / 8), words);
+      reinterpret_cast<uint32_t*>(c.v_meta)[vbh * d + ch] = (uint32_t)mb | ((uint32_t)sb << 16);
+      store_sum(c.v_sums, vbh * d + ch, c.sum_bytes, sum);
     }
   }
-  __syncthreads();
+  __syncthreads();  // every thread has read lens[s]
   if (threadIdx.x == 0) lens[s] = L + 1;
 }
 

@@ -230,3 +230,30 @@ def hack_debug_pv_products(layout, cache: KVCache, p_codes: torch.Tensor, p_meta
                                         hq, _dev(seq_lens, torch.int32, "seq_lens"), batch, max_len,
                                         prod.data_ptr(), out.data_ptr(), _stream(stream)), "hack_debug_pv_products")
     return prod, out
+
+
+class BoundCall:
+    """A library call with its arguments marshalled once (for tight loops): calling
+    it passes the prepared ctypes arguments and the current stream."""
+
+    def __init__(self, fn_name: str, where: str, *args):
+        self._fn = getattr(lib(), fn_name)
+        self._args = args
+        self._where = where
+
+    def __call__(self, stream=None):
+        _check(self._fn(*self._args, _stream(stream)), self._where)
+
+
+def bind_append(layout, cache: KVCache, k_new, v_new, seq_lens, max_len: int, tail_mode: int = TAIL_FP16):
+    return BoundCall("hack_append", "hack_append", ctypes.byref(layout), ctypes.byref(cache.struct),
+                     _dev(k_new, torch.float16, "k_new"), _dev(v_new, torch.float16, "v_new"),
+                     _dev(seq_lens, torch.int32, "seq_lens"), k_new.shape[0], max_len, tail_mode)
+
+
+def bind_attend_decode(layout, cache: KVCache, q, seq_lens, max_len: int, tail_mode: int, out, workspace):
+    batch, hq, _ = q.shape
+    return BoundCall("hack_attend_decode", "hack_attend_decode", ctypes.byref(layout), ctypes.byref(cache.struct),
+                     _dev(q, torch.float16, "q"), hq, _dev(seq_lens, torch.int32, "seq_lens"), batch, max_len,
+                     tail_mode, _dev(out, torch.float32, "out"), _dev(workspace, torch.uint8, "workspace"),
+                     workspace.numel())
