@@ -58,7 +58,22 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prefill", action="store_true")
     ap.add_argument("--prefill-iters", type=int, default=10)
+    ap.add_argument("--only", choices=["decode", "prefill", "copy"], default=None,
+                    help="profiling aid: run one leg alone (copy = plain device copy of a known size, "
+                         "the calibration for HBM byte counters)")
     return ap.parse_args()
+
+
+def copy_calibration(mib: int = 512, iters: int = 5):
+    """A plain device-to-device copy of `mib` MiB, `iters` times: a kernel whose HBM
+    traffic is known exactly (mib MiB read + mib MiB written per launch)."""
+    import torch
+    src = torch.ones(mib << 18, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(iters):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_mib": mib, "launches": iters}), flush=True)
 
 
 def cpu_baseline_decode(wl, budget_s: float = 15.0):
@@ -94,6 +109,12 @@ def main():
               f"(sequence, kv head) with no communication, so N GPUs run N independent copies.",
               file=sys.stderr)
         sys.exit(2)
+    if args.only == "copy":
+        copy_calibration()
+        return
+    if args.only == "prefill":
+        print(json.dumps({"prefill": bench_prefill(args.prefill_iters)}), flush=True)
+        return
     import torch
     from paper_2502_03589_amd import hack as hk
     from paper_2502_03589_amd import synth
@@ -198,9 +219,9 @@ def main():
                      "traffic": None, "avg_kernel_us": round(avg_kern_ms * 1e3, 3),
                      "bytes_per_launch": int(np.mean(dec_bytes))},
     }
-    if not args.no_prefill:
+    if not args.no_prefill and args.only is None:
         result["prefill"] = bench_prefill(args.prefill_iters)
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.only is None:
         result["cpu_baseline"] = cpu_baseline_decode(wl)
     print(json.dumps(result), flush=True)
 

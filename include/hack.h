@@ -160,8 +160,8 @@ int64_t hack_decode_workspace_bytes(const hack_kv_layout* layout, int32_t batch,
  * hack_decode_workspace_bytes(...) bytes (no initialization needed) and must not
  * be shared by calls that may run concurrently.  One or two kernels are launched
  * (the second merges the chunks of long sequences).
- * Requires head_dim 128, partition 32 or 64, and H_q/H_kv <= 8 (else
- * HACK_ERR_UNSUPPORTED). */
+ * Requires head_dim 128, partition 32 or 64, H_q/H_kv <= 8 and, for a paged cache,
+ * page_tokens a multiple of 4 * partition (else HACK_ERR_UNSUPPORTED). */
 hack_status hack_attend_decode(const hack_kv_layout* layout, const hack_kv_cache* cache,
                                const void* q_dev, int32_t num_q_heads, const int32_t* seq_lens_dev,
                                int32_t batch, int32_t max_len, int32_t tail_mode, float* out_dev,

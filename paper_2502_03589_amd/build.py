@@ -17,6 +17,8 @@ FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     # keep MFMA accumulators in VGPRs: the kernels update them with VALU ops too
     "-mllvm", "-amdgpu-mfma-vgpr-form",
+    # inputs carry no NaNs (a caller contract): min/max need no quieting of operands
+    "-fno-honor-nans",
 ]
 
 

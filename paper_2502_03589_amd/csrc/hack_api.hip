@@ -158,6 +158,8 @@ static hack_status decode_common(const hack_kv_layout* layout, const hack_kv_cac
   const int64_t cap = cache_capacity(layout, cache, batch);
   if (cap < 0) return HACK_ERR_INVALID_ARGUMENT;
   if (max_len > cap) return HACK_ERR_CAPACITY;
+  // a decode span (four V blocks) must not cross a page
+  if (cache->block_table_dev && layout->page_tokens % (4 * layout->partition) != 0) return HACK_ERR_UNSUPPORTED;
   std::memset(&a, 0, sizeof(a));
   a.c = make_view(layout, cache);
   a.q = static_cast<const __half*>(q_dev);

@@ -139,13 +139,16 @@ __device__ __forceinline__ uint64_t element_index(int s, int kv_heads, int h, in
 // ---------------------------------------------------------------------------
 // Cross-lane reductions inside a row of 16 lanes (DPP row rotates).
 // ---------------------------------------------------------------------------
+// Every lane of a row rotate has a source in its own row, so the bound-control
+// form changes nothing; it lets the compiler fold the move into the ALU op that
+// consumes it (v_max_f32_dpp, v_add_f32_dpp, ...).
 template <int CTRL>
 __device__ __forceinline__ float dpp_f(float x) {
-  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xF, 0xF, false));
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, true));
 }
 template <int CTRL>
 __device__ __forceinline__ int dpp_i(int x) {
-  return __builtin_amdgcn_mov_dpp(x, CTRL, 0xF, 0xF, false);
+  return __builtin_amdgcn_update_dpp(0, x, CTRL, 0xF, 0xF, true);
 }
 
 // row_ror:n has DPP control 0x120 + n.

@@ -2,19 +2,19 @@
 //
 // Work split: one workgroup of four 64-lane wavefronts per (sequence, kv head,
 // chunk of the context); wave w takes spans w, w+4, ... of the chunk, where a span
-// is four V blocks (4*PI tokens).  Every global load of a span is issued before
-// any of its arithmetic.  Per span a wave computes, for up to 4 query heads of
-// the kv group per row tile:
-//   Q'K'  v_mfma_i32_16x16x64_i8: A = 8-bit Q codes (minus 128), rows = (channel
-//         quarter q, head h), block-diagonal so that lane group g only carries
-//         quarter g; B = 2/4-bit K codes unpacked in registers (lane = token,
-//         group = quarter).  Lane (t, g) receives the products of quarter g for the
-//         4 heads.
-//   Eq. 4 the rank-1 terms (m~_q * s_k sum k' and R_q * m_k) come from two
-//         v_mfma_f32_16x16x4_f32 (block-diagonal A of Q constants, B = the lane's
-//         own K partition metadata); the product term s_q s_k C~ is on the VALU.
-//         A permlane reduce-scatter sums the quarters so that lane (t, g) holds the
-//         score of head g (log2 units).
+// is four V blocks (4*PI tokens) that lie in one page.  Every global load of a span
+// is issued before any of its arithmetic, from wave-uniform section bases plus
+// fixed per-lane offsets.  Per span a wave computes, for up to 4 query heads of the
+// kv group per row tile:
+//   Q'K'  v_mfma_i32_16x16x64_i8: A = 8-bit Q codes (minus 128) with rows
+//         (head h, channel quarter q), block-diagonal so that lane group g only
+//         carries quarter g; B = 2/4-bit K codes unpacked in registers (lane = token,
+//         group = quarter).  Lane (t, g) receives the four quarter products of head g.
+//   Eq. 4 v_mfma_f32_16x16x4_f32 with B = the lane's own K partition metadata
+//         spreads it over the output layout: one product gives s_q s_k per
+//         (head, quarter), two more give the rank-1 terms (m~_q s_k sum k' and
+//         R_q m_k) already summed over the partitions.  The VALU only converts the
+//         integer products and takes four fused multiply-adds per score (log2 units).
 //   softmax online with a lazily raised reference max; P quantized to 8 bits per
 //         V block (min, scale, round-to-nearest-even codes), staged through LDS.
 //   P'V'  v_mfma_i32_16x16x64_i8: A = P codes, rows = (block, head) block-diagonal
@@ -88,8 +88,8 @@ __device__ __forceinline__ v4f mfma_f32(float a, float b, v4f c) {
 __device__ __forceinline__ float lo_half(uint32_t w) { return __half2float(__ushort_as_half((uint16_t)(w & 0xFFFFu))); }
 __device__ __forceinline__ float hi_half(uint32_t w) { return __half2float(__ushort_as_half((uint16_t)(w >> 16))); }
 
-// Sum four per-quarter partial values over the four lane groups so that lane
-// group g ends with the total of value g (permlane swaps across 32 and 16 lanes).
+// Sum four per-lane values over the four lane groups so that lane group g ends
+// with the total of value g (permlane swaps across 32 and 16 lanes).
 __device__ __forceinline__ float reduce_scatter4(float v0, float v1, float v2, float v3) {
   const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(v0), __float_as_uint(v2), false, false);
   const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v1), __float_as_uint(v3), false, false);
@@ -110,80 +110,128 @@ constexpr float kScoreScale = 0.12751743074941640f;
 constexpr float kMaxSlack = 8.0f;
 
 constexpr int kWaves = 4;
+constexpr int kComputeUnits = 256;  // MI355X
 
-#ifndef HACK_DECODE_PREFETCH
-#define HACK_DECODE_PREFETCH 0
-#endif
-#ifndef HACK_DECODE_WAVES_PER_SIMD
-#define HACK_DECODE_WAVES_PER_SIMD 2
-#endif
-#ifndef HACK_DECODE_TARGET_WGS
-#define HACK_DECODE_TARGET_WGS 512
+// Bytes of one cached code sum: 1 when b + ceil(log2 PI) <= 8, else 2 (Sec. 5.3).
+template <int BITS, int PI>
+constexpr int sum_width() {
+  int need = BITS;
+  for (int v = 1; v < PI; v <<= 1) ++need;
+  return need <= 8 ? 1 : 2;
+}
+
+// Waves per SIMD the register budget is sized for.  The 2-bit, partition-32
+// kernel with one row tile fits in 128 VGPRs (four waves per SIMD hide the load
+// latency of a span behind three others' arithmetic); wider spans and two row
+// tiles need more registers.
+template <int BITS, int PI, int GT>
+constexpr int decode_occupancy() {
+  return (BITS == 2 && PI == 32 && GT == 1) ? 4 : 2;
+}
+
+#ifndef HACK_DECODE_WGS_PER_CU
+#define HACK_DECODE_WGS_PER_CU 0  // 0: the kernel's occupancy
 #endif
 
-// Cache addresses of the four V blocks of a span (wave-uniform): the row of each
-// block's first token in the K sections and the block's index in the V sections.
-struct SpanAddr {
-  int64_t krow[4];
-  int64_t vblk[4];
+// Section bases of a span: its four V blocks are consecutive blocks of one page.
+struct SpanBase {
+  const uint8_t* kc;
+  const uint8_t* km;
+  const uint8_t* kz;
+  const uint8_t* vc;
+  const uint8_t* vm;
+  const uint8_t* vz;
 };
 
-template <int PI>
-__device__ __forceinline__ void span_addresses(const CacheView& c, int s, int hkv, int span0, int L,
-                                               SpanAddr& ad) {
-  const int bpp = c.page_tokens / PI;  // blocks per page
-  const int kb0 = span0 / PI;
-  int pidx = 0, slot = kb0;
+template <int BITS, int PI>
+__device__ __forceinline__ SpanBase span_base(const CacheView& c, int s, int hkv, int span0) {
+  constexpr int D = 128, P = D / PI, SB = sum_width<BITS, PI>();
+  int64_t page;
+  int slot0;
   if (c.block_table) {
-    pidx = kb0 / bpp;
-    slot = kb0 - pidx * bpp;
+    const int pidx = span0 / c.page_tokens;
+    const int64_t pg = c.block_table[(int64_t)s * c.mbps + pidx];
+    page = pg < 0 ? 0 : (pg >= c.num_pages ? c.num_pages - 1 : pg);
+    slot0 = span0 - pidx * c.page_tokens;
+  } else {
+    page = s < c.num_pages ? s : c.num_pages - 1;
+    slot0 = span0;
   }
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    int64_t page = 0;
-    if (span0 + k * PI < L) {
-      if (c.block_table) {
-        int64_t pg = c.block_table[(int64_t)s * c.mbps + pidx];
-        page = pg < 0 ? 0 : (pg >= c.num_pages ? c.num_pages - 1 : pg);
-      } else {
-        page = s < c.num_pages ? s : c.num_pages - 1;
-      }
-    }
-    ad.krow[k] = (page * c.kv_heads + hkv) * c.page_tokens + (int64_t)slot * PI;
-    ad.vblk[k] = (page * c.kv_heads + hkv) * bpp + slot;
-    if (++slot == bpp && c.block_table) {
-      slot = 0;
-      ++pidx;
-    }
-  }
+  const int64_t krow = (page * c.kv_heads + hkv) * c.page_tokens + slot0;
+  const int64_t vblk = (page * c.kv_heads + hkv) * (c.page_tokens / PI) + slot0 / PI;
+  SpanBase b;
+  b.kc = c.k_codes + krow * (D * BITS / 8);
+  b.km = reinterpret_cast<const uint8_t*>(c.k_meta) + krow * (P * 4);
+  b.kz = c.k_sums + krow * (P * SB);
+  b.vc = c.v_codes + vblk * (D * (PI * BITS / 8));
+  b.vm = reinterpret_cast<const uint8_t*>(c.v_meta) + vblk * (D * 4);
+  b.vz = c.v_sums + vblk * (D * SB);
+  return b;
 }
 
 // Register copy of one span's compressed data for one lane.
 template <int BITS, int PI>
 struct SpanData {
   static constexpr int NT = PI / 4;              // 16-token tiles per span
-  static constexpr int KW = BITS;                // K dwords per (token, quarter)
   static constexpr int VW = PI * BITS / 32;      // V dwords per (channel, block)
-  uint32_t kc[NT][KW];  // K codes of the lane's token and channel quarter, per tile
-  uint32_t km[NT];      // (m_k, s_k) of the lane's K partition, per tile
-  uint32_t kz[NT];      // cached code sum of that partition, per tile
-  uint32_t vc[8 * VW];  // V codes of 8 channels of the lane's block
-  uint32_t vm[8];       // (m_v, s_v) of those channels
-  uint32_t vz[8];       // cached V code sums
+  static constexpr int SB = sum_width<BITS, PI>();
+  uint32_t kc[NT][BITS];  // K codes of the lane's token and channel quarter, per tile
+  uint32_t km[NT];        // (m_k, s_k) of the lane's K partition, per tile
+  uint32_t kz[NT];        // cached code sum of that partition, per tile
+  uint32_t vc[8 * VW];    // V codes of 8 channels of the lane's block
+  uint32_t vm[8];         // (m_v, s_v) of those channels
+  uint32_t vz[2 * SB];    // cached V code sums of those channels, packed
 };
 
+// V of one span staged in LDS by direct global->LDS loads: copy i of the codes
+// holds bytes [16i, 16i+16) of every lane's run, lane-major, so that each lane
+// reads its own 16-byte pieces back without bank conflicts.
+template <int BITS, int PI>
+struct VStage {
+  static constexpr int VW = PI * BITS / 32;
+  static constexpr int SB = sum_width<BITS, PI>();
+  static constexpr int NC = 8 * VW / 4;               // 16-byte pieces of V codes per lane
+  static constexpr int ZB = SB == 1 ? 4 : 16;         // bytes per sum piece
+  static constexpr int NZ = 8 * SB / ZB;              // sum pieces per lane
+  uint8_t codes[NC][64 * 16];
+  uint8_t meta[2][64 * 16];
+  uint8_t sums[NZ][64 * ZB];
+};
+
+// Whether a kernel stages V through LDS (the four-waves-per-SIMD configuration,
+// whose register budget cannot also hold a span's V data).
+template <int BITS, int PI, int GT>
+constexpr bool decode_v_in_lds() {
+  return decode_occupancy<BITS, PI, GT>() == 4;
+}
+
 // LDS of one wave.
-template <int PI, int GT>
+template <int BITS, int PI, int GT>
 struct WaveLds {
+  static constexpr int HT = 4 * GT;
   int8_t p[GT][4][4][PI];       // P codes - 128: [row tile][block][head][token position]
   float pst[GT][4][2][4];       // [rt][block][s_p | m~_p][head], scaled to the span's reference max
   float alpha[GT][4];           // O rescale of the span, per head
   float tailf[GT][4];           // scale of the fp16 open block's probabilities
   float ptail[GT][4][PI];       // unquantized p~ of the open block
+  // the wave's V staging; after its last span the wave's partial O reuses the space
+  union {
+    VStage<BITS, PI> vst[decode_v_in_lds<BITS, PI, GT>() ? 1 : 0];
+    float mrg_o[HT][128];
+  };
 };
 
+__device__ __forceinline__ void lds_dma16(const uint8_t* src, uint8_t* lds) {
+  __builtin_amdgcn_global_load_lds((__attribute__((address_space(1))) const void*)src,
+                                   (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+}
+__device__ __forceinline__ void lds_dma4(const uint8_t* src, uint8_t* lds) {
+  __builtin_amdgcn_global_load_lds((__attribute__((address_space(1))) const void*)src,
+                                   (__attribute__((address_space(3))) void*)lds, 4, 0, 0);
+}
+
 template <int BITS, int PI, int GT, int MODE>
-__global__ __launch_bounds__(256, HACK_DECODE_WAVES_PER_SIMD) void decode_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decode_kernel(DecodeArgs a) {
   constexpr int D = 128;
   constexpr int P = D / PI;          // K partitions per token
   constexpr int QPP = 4 / P;         // channel quarters per partition
@@ -193,12 +241,16 @@ __global__ __launch_bounds__(256, HACK_DECODE_WAVES_PER_SIMD) void decode_kernel
   constexpr int KW = BITS;           // K code dwords per (token, quarter of 32 channels)
   constexpr int VW = PI * BITS / 32; // V code dwords per (channel, block)
   constexpr int SW = BITS / 2;       // dwords per 16-code slice
+  constexpr int SB = sum_width<BITS, PI>();
   constexpr int HT = GT * 4;
+  constexpr int KROW = D * BITS / 8; // K code bytes per token
 
-  __shared__ int8_t q_lds[HT][D];
+  // Q codes - 128 per (head slot, quarter, 16-channel slice), each slice already in
+  // the byte order of the K operand's in-register unpack
+  __shared__ __attribute__((aligned(16))) int8_t q_lds[HT][4][2][16];
   __shared__ float qm_lds[HT][4][3];
-  __shared__ __attribute__((aligned(16))) WaveLds<PI, GT> wl_all[kWaves];
-  __shared__ float mrg_o[kWaves][HT][D];
+  constexpr bool VLDS = decode_v_in_lds<BITS, PI, GT>();
+  __shared__ __attribute__((aligned(16))) WaveLds<BITS, PI, GT> wl_all[kWaves];
   __shared__ float mrg_ml[kWaves][HT][2];
 
   const CacheView& c = a.c;
@@ -222,7 +274,7 @@ __global__ __launch_bounds__(256, HACK_DECODE_WAVES_PER_SIMD) void decode_kernel
   const int nsplit = (L + a.chunk - 1) / a.chunk;
   const int F = L / PI, T = L - F * PI;
   const bool requant = a.tail_requant != 0;
-  WaveLds<PI, GT>& wl = wl_all[wave];
+  WaveLds<BITS, PI, GT>& wl = wl_all[wave];
 
   // ---- Q: 8-bit codes per partition with float32 metadata (Sec. 5.1, Sec. 5.2) ----
   // wave w quantizes head slots w, w+4, ...; each lane holds two channels
@@ -255,8 +307,12 @@ __global__ __launch_bounds__(256, HACK_DECODE_WAVES_PER_SIMD) void decode_kernel
       int csum = (int)c0 + (int)c1;
 #pragma unroll
       for (int m = 1; m < PI / 2; m <<= 1) csum += __shfl_xor(csum, m, 64);
-      q_lds[gh][2 * lane] = real ? (int8_t)((int)c0 - 128) : (int8_t)0;
-      q_lds[gh][2 * lane + 1] = real ? (int8_t)((int)c1 - 128) : (int8_t)0;
+      {
+        const int ch = 2 * lane;  // channels ch, ch + 1 share quarter and slice
+        const int g = ch >> 5, m = (ch >> 4) & 1, e = ch & 15;
+        q_lds[gh][g][m][perm_position<BITS>(e)] = real ? (int8_t)((int)c0 - 128) : (int8_t)0;
+        q_lds[gh][g][m][perm_position<BITS>(e + 1)] = real ? (int8_t)((int)c1 - 128) : (int8_t)0;
+      }
       const int p = (2 * lane) / PI;
       if ((2 * lane) % PI == 0) {
         // per partition: s_q, m~_q = m_q + 128 s_q, R = s_q sum q' + n m_q (all in log2 units)
@@ -276,35 +332,28 @@ __global__ __launch_bounds__(256, HACK_DECODE_WAVES_PER_SIMD) void decode_kernel
   }
   __syncthreads();
 
-  // Q operands.  Rows of the QK tile are (quarter q, head h) = 4q + h; lane (row, group g)
-  // is non-zero only for q == g.  qa: int8 codes; ra: the rank-1 coefficients of Eq. 4
-  // (m~_q and R, divided among the QPP quarters of a partition); sq_: s_q of the lane's
-  // quarter for head i, used by the product term.
+  // Q operands.  Rows of the QK tile are (head h, quarter q) = 4h + q; the i8
+  // operand of lane (row, group g) is non-zero only for q == g.  The f32 operands
+  // take the lane's group as the summed index k: qs = s_q of (h, quarter k) on the
+  // diagonal q == k, so s_q s_k lands at (lane group h, register q); ra0 / ra1 =
+  // m~_q and R of (h, partition of quarter k), divided among the QPP quarters of a
+  // partition, so that the rank-1 terms arrive summed over the partitions.
   v4i qa[GT][2];
-  float ra[GT][2];
-  float sq_[GT][4];
+  float qs[GT], ra0[GT], ra1[GT];
   const int pl = grp / QPP;  // partition of this lane's quarter
   if constexpr (MODE != MODE_PV) {
-    const int qq = col >> 2, hh = col & 3;
+    const int hh = col >> 2, qq = col & 3;
 #pragma unroll
     for (int rt = 0; rt < GT; ++rt) {
 #pragma unroll
       for (int m = 0; m < 2; ++m) {
-        int b4[4] = {0, 0, 0, 0};
-        if (qq == grp) {
-#pragma unroll
-          for (int bp = 0; bp < 16; ++bp) {
-            const int v = (int)(uint8_t)q_lds[rt * 4 + hh][32 * grp + 16 * m + perm_offset<BITS>(bp)];
-            b4[bp >> 2] |= v << (8 * (bp & 3));
-          }
-        }
-        qa[rt][m] = v4i{b4[0], b4[1], b4[2], b4[3]};
+        const int4 w = *reinterpret_cast<const int4*>(&q_lds[rt * 4 + hh][grp][m][0]);
+        qa[rt][m] = qq == grp ? v4i{w.x, w.y, w.z, w.w} : v4i{0, 0, 0, 0};
       }
       constexpr float inv_qpp = 1.0f / (float)QPP;
-      ra[rt][0] = qq == grp ? qm_lds[rt * 4 + hh][pl][1] * inv_qpp : 0.0f;
-      ra[rt][1] = qq == grp ? qm_lds[rt * 4 + hh][pl][2] * inv_qpp : 0.0f;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) sq_[rt][i] = qm_lds[rt * 4 + i][pl][0];
+      qs[rt] = qq == grp ? qm_lds[rt * 4 + hh][pl][0] : 0.0f;
+      ra0[rt] = qm_lds[rt * 4 + hh][pl][1] * inv_qpp;
+      ra1[rt] = qm_lds[rt * 4 + hh][pl][2] * inv_qpp;
     }
   }
 
@@ -319,27 +368,32 @@ __global__ __launch_bounds__(256, HACK_DECODE_WAVES_PER_SIMD) void decode_kernel
   }
 
   const int nspan = (t1 - t0 + SPAN - 1) / SPAN;
-  const uint32_t k_lane_off = (uint32_t)(col * (D * BITS / 8) + grp * (32 * BITS / 8));
+  // per-lane byte offsets inside a span's sections (tile ti adds ti * 16 rows)
+  const uint32_t kc_off = (uint32_t)(col * KROW + grp * (32 * BITS / 8));
+  const uint32_t km_off = (uint32_t)((col * P + pl) * 4);
+  const uint32_t kz_off = (uint32_t)((col * P + pl) * SB);
+  const uint32_t vc_off = (uint32_t)((grp * D + 8 * col) * (PI * BITS / 8));
+  const uint32_t vm_off = (uint32_t)((grp * D + 8 * col) * 4);
+  const uint32_t vz_off = (uint32_t)((grp * D + 8 * col) * SB);
 
-  // Full spans (every token valid, every block quantized) are software-pipelined:
-  // the loads of a wave's next span are in flight while it computes the current one.
-  // At most one span per chunk, its last, is partial; it takes the masked path.
+  // Spans whose tokens are all valid and whose blocks are all quantized take the
+  // unmasked path; at most one span per chunk, its last, is partial.
   const int nspan_full = max(0, min(nspan, (F * PI - t0) / SPAN));
   auto load_span = [&](SpanData<BITS, PI>& d, int span0, auto masked_tag) __attribute__((always_inline)) {
     constexpr bool MASKED = decltype(masked_tag)::value;
     constexpr bool full = !MASKED;
-    SpanAddr ad;
-    span_addresses<PI>(c, s, hkv, span0, L, ad);
-    // ---------------- global loads of the whole span ----------------
+    const SpanBase b = span_base<BITS, PI>(c, s, hkv, span0);
+    // the offsets stay 32-bit values next to each load (not hoisted and widened), so
+    // every load takes the scalar-base + 32-bit-offset + immediate form
+    uint32_t o_kc = kc_off, o_km = km_off, o_kz = kz_off, o_vc = vc_off, o_vm = vm_off, o_vz = vz_off;
+    asm volatile("" : "+v"(o_kc), "+v"(o_km), "+v"(o_kz), "+v"(o_vc), "+v"(o_vm), "+v"(o_vz));
 #pragma unroll
     for (int ti = 0; ti < NT; ++ti) {
-      const int tb = span0 + 16 * ti;  // first token of the tile (wave-uniform)
-      const int64_t row0 = ad.krow[ti / TILES] + 16 * (ti % TILES);
-      if (full || tb + col < L) {
-        load_words<KW>(c.k_codes + row0 * (D * BITS / 8) + k_lane_off, d.kc[ti]);
-        const uint32_t mi = (uint32_t)(col * P + pl);
-        d.km[ti] = reinterpret_cast<const uint32_t*>(c.k_meta)[row0 * P + mi];
-        d.kz[ti] = load_sum(c.k_sums + row0 * P * c.sum_bytes, mi, c.sum_bytes);
+      if (full || span0 + 16 * ti + col < L) {
+        load_words<KW>(b.kc + o_kc + ti * 16 * KROW, d.kc[ti]);
+        d.km[ti] = *reinterpret_cast<const uint32_t*>(b.km + o_km + ti * 16 * P * 4);
+        if constexpr (SB == 1) d.kz[ti] = b.kz[o_kz + ti * 16 * P];
+        else d.kz[ti] = *reinterpret_cast<const uint16_t*>(b.kz + o_kz + ti * 16 * P * 2);
       } else {
 #pragma unroll
         for (int w = 0; w < KW; ++w) d.kc[ti][w] = 0u;
@@ -352,33 +406,32 @@ __global__ __launch_bounds__(256, HACK_DECODE_WAVES_PER_SIMD) void decode_kernel
     const int vkb = vbt0 / PI;
     bool gvalid = full || (vbt0 < L && (vkb < F || (requant && vkb == F && T > 0)));
     if constexpr (MODE == MODE_PV) gvalid = vbt0 < L && vkb < F;
+    if constexpr (VLDS) {
+      // straight into this wave's LDS; lanes of blocks that are not read leave
+      // their slots stale and zero their values when reading them back
+      using VS = VStage<BITS, PI>;
+      if (gvalid) {
 #pragma unroll
-    for (int w = 0; w < 8 * VW; ++w) d.vc[w] = 0u;
+        for (int i = 0; i < VS::NC; ++i) lds_dma16(b.vc + o_vc + 16 * i, wl.vst[0].codes[i]);
 #pragma unroll
-    for (int j = 0; j < 8; ++j) d.vm[j] = d.vz[j] = 0u;
-    if (gvalid) {
-      const int64_t vb = grp == 0 ? ad.vblk[0] : (grp == 1 ? ad.vblk[1] : (grp == 2 ? ad.vblk[2] : ad.vblk[3]));
-      load_words<8 * VW>(c.v_codes + (vb * D + 8 * col) * (PI * BITS / 8), d.vc);
-      const uint4* mp = reinterpret_cast<const uint4*>(c.v_meta + vb * D + 8 * col);
-      const uint4 m0 = mp[0], m1 = mp[1];
-      d.vm[0] = m0.x; d.vm[1] = m0.y; d.vm[2] = m0.z; d.vm[3] = m0.w;
-      d.vm[4] = m1.x; d.vm[5] = m1.y; d.vm[6] = m1.z; d.vm[7] = m1.w;
-      if (c.sum_bytes == 1) {
-        const uint2 z = *reinterpret_cast<const uint2*>(c.v_sums + vb * D + 8 * col);
+        for (int i = 0; i < 2; ++i) lds_dma16(b.vm + o_vm + 16 * i, wl.vst[0].meta[i]);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          d.vz[j] = (z.x >> (8 * j)) & 0xFFu;
-          d.vz[4 + j] = (z.y >> (8 * j)) & 0xFFu;
-        }
-      } else {
-        const uint4 z = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(c.v_sums) + vb * D + 8 * col);
-        const uint32_t zz[4] = {z.x, z.y, z.z, z.w};
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          d.vz[2 * j] = zz[j] & 0xFFFFu;
-          d.vz[2 * j + 1] = zz[j] >> 16;
+        for (int i = 0; i < VS::NZ; ++i) {
+          if constexpr (VS::ZB == 4) lds_dma4(b.vz + o_vz + 4 * i, wl.vst[0].sums[i]);
+          else lds_dma16(b.vz + o_vz + 16 * i, wl.vst[0].sums[i]);
         }
       }
+    } else if (gvalid) {
+      load_words<8 * VW>(b.vc + o_vc, d.vc);
+      load_words<8>(b.vm + o_vm, d.vm);
+      load_words<2 * SB>(b.vz + o_vz, d.vz);
+    } else {
+#pragma unroll
+      for (int w = 0; w < 8 * VW; ++w) d.vc[w] = 0u;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) d.vm[j] = 0u;
+#pragma unroll
+      for (int j = 0; j < 2 * SB; ++j) d.vz[j] = 0u;
     }
   };
   auto compute_span = [&](const SpanData<BITS, PI>& d, int span0, auto masked_tag) __attribute__((always_inline)) {
@@ -450,33 +503,31 @@ __global__ __launch_bounds__(256, HACK_DECODE_WAVES_PER_SIMD) void decode_kernel
             v4i acc = v4i{0, 0, 0, 0};
             acc = mfma_i8(qa[rt][0], b0, acc);
             acc = mfma_i8(qa[rt][1], b1, acc);
+            const v4f sqk = mfma_f32(qs[rt], skv, v4f{0.0f, 0.0f, 0.0f, 0.0f});  // s_q s_k per quarter
             v4f rk = v4f{0.0f, 0.0f, 0.0f, 0.0f};
-            rk = mfma_f32(ra[rt][0], bz, rk);   // m~_q * s_k * sum k'
-            rk = mfma_f32(ra[rt][1], mk, rk);   // R_q * m_k
-            float part[4];
+            rk = mfma_f32(ra0[rt], bz, rk);   // sum over partitions of m~_q s_k sum k'
+            rk = mfma_f32(ra1[rt], mk, rk);   // sum over partitions of R_q m_k
+            float sc = rk[0];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) part[i] = fmaf(sq_[rt][i] * skv, (float)acc[i], rk[i]);
+            for (int q = 0; q < 4; ++q) sc = fmaf((float)acc[q], sqk[q], sc);
             if constexpr (MODE == MODE_QK) {
-              // integer partition products (unsigned codes) for the test export
-              int cp[4];
-#pragma unroll
-              for (int i = 0; i < 4; ++i) {
-                int v = acc[i];
-                if constexpr (QPP >= 2) v += __shfl_xor(v, 16, 64);
-                if constexpr (QPP >= 4) v += __shfl_xor(v, 32, 64);
-                cp[i] = v + 128 * (int)d.kz[ti];
-              }
+              // integer partition products (unsigned codes) for the test export:
+              // quarter q's code sum comes from lane (token, q)
               const int tok = bt0 + 16 * tl + col;
-              if (tok < L && grp % QPP == 0) {
+              const int gh = rt * 4 + grp;
+              int zq[P];
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                  const int gh = rt * 4 + i;
-                  if (gh < G)
-                    a.dbg_prod[(((int64_t)s * Hq + hkv * G + gh) * a.max_len + tok) * P + pl] = cp[i];
+              for (int p = 0; p < P; ++p) zq[p] = __shfl((int)d.kz[ti], 16 * (p * QPP) + col, 64);
+              if (tok < L && gh < G) {
+#pragma unroll
+                for (int p = 0; p < P; ++p) {
+                  int v = 128 * zq[p];
+#pragma unroll
+                  for (int q = p * QPP; q < (p + 1) * QPP; ++q) v += acc[q];
+                  a.dbg_prod[(((int64_t)s * Hq + hkv * G + gh) * a.max_len + tok) * P + p] = v;
                 }
               }
             }
-            const float sc = reduce_scatter4(part[0], part[1], part[2], part[3]);
             sv[rt][tl] = (full || bt0 + 16 * tl + col < L) ? sc : -INFINITY;
           }
         }
@@ -554,11 +605,42 @@ __global__ __launch_bounds__(256, HACK_DECODE_WAVES_PER_SIMD) void decode_kernel
 
     // ---------------- P'V' and Eq. 4: lane (channel col, group = block k) ----------------
     {
+      uint32_t vcr[8 * VW], vmr[8], vzr[2 * SB];
+      if constexpr (VLDS) {
+        using VS = VStage<BITS, PI>;
+        // the direct-to-LDS loads of this span have landed once vmcnt is zero
+        __builtin_amdgcn_s_waitcnt(0x0F70);
+#pragma unroll
+        for (int i = 0; i < VS::NC; ++i) {
+          const uint4 x = gvalid ? *reinterpret_cast<const uint4*>(&wl.vst[0].codes[i][16 * lane]) : uint4{0, 0, 0, 0};
+          vcr[4 * i] = x.x; vcr[4 * i + 1] = x.y; vcr[4 * i + 2] = x.z; vcr[4 * i + 3] = x.w;
+        }
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          const uint4 x = gvalid ? *reinterpret_cast<const uint4*>(&wl.vst[0].meta[i][16 * lane]) : uint4{0, 0, 0, 0};
+          vmr[4 * i] = x.x; vmr[4 * i + 1] = x.y; vmr[4 * i + 2] = x.z; vmr[4 * i + 3] = x.w;
+        }
+#pragma unroll
+        for (int i = 0; i < VS::NZ; ++i) {
+          if constexpr (VS::ZB == 4) {
+            vzr[i] = gvalid ? *reinterpret_cast<const uint32_t*>(&wl.vst[0].sums[i][4 * lane]) : 0u;
+          } else {
+            const uint4 x = gvalid ? *reinterpret_cast<const uint4*>(&wl.vst[0].sums[i][16 * lane]) : uint4{0, 0, 0, 0};
+            vzr[4 * i] = x.x; vzr[4 * i + 1] = x.y; vzr[4 * i + 2] = x.z; vzr[4 * i + 3] = x.w;
+          }
+        }
+      } else {
+#pragma unroll
+        for (int w = 0; w < 8 * VW; ++w) vcr[w] = d.vc[w];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) vmr[j] = d.vm[j];
+#pragma unroll
+        for (int j = 0; j < 2 * SB; ++j) vzr[j] = d.vz[j];
+      }
       const float n_g = (float)(vkb < F ? PI : T);
       const int kk = col >> 2, hh = col & 3;
       v4i pa[GT][TILES];
-      float sp_[GT][4];
-      float pr1[GT], pr2[GT];
+      float pr0[GT], pr1[GT], pr2[GT];
 #pragma unroll
       for (int rt = 0; rt < GT; ++rt) {
 #pragma unroll
@@ -570,8 +652,6 @@ __global__ __launch_bounds__(256, HACK_DECODE_WAVES_PER_SIMD) void decode_kernel
             pa[rt][sl] = v4i{0, 0, 0, 0};
           }
         }
-        const float4 f0 = *reinterpret_cast<const float4*>(&wl.pst[rt][grp][0][0]);
-        sp_[rt][0] = f0.x; sp_[rt][1] = f0.y; sp_[rt][2] = f0.z; sp_[rt][3] = f0.w;
         if constexpr (MODE != MODE_PV) {
           const float4 al = *reinterpret_cast<const float4*>(&wl.alpha[rt][0]);
           if (al.x != 1.0f || al.y != 1.0f || al.z != 1.0f || al.w != 1.0f) {
@@ -588,30 +668,36 @@ __global__ __launch_bounds__(256, HACK_DECODE_WAVES_PER_SIMD) void decode_kernel
         const float zp[4] = {(float)sacc[0], (float)sacc[1], (float)sacc[2], (float)sacc[3]};
         // rank-1 coefficients, block-diagonal: lane (row kk*4+hh, group g) non-zero for kk == g
         // (such a lane's own registers hold the sums of block g = kk)
-        pr1[rt] = kk == grp ? wl.pst[rt][kk][0][hh] * pick4(zp, hh) : 0.0f;  // s_p * sum p~'
+        pr0[rt] = kk == grp ? wl.pst[rt][kk][0][hh] : 0.0f;                  // s_p
+        pr1[rt] = pr0[rt] * pick4(zp, hh);                                   // s_p * sum p~'
         pr2[rt] = kk == grp ? wl.pst[rt][kk][1][hh] : 0.0f;                 // m~_p = m_p + 128 s_p
       }
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        const float mv = lo_half(d.vm[j]), svj = hi_half(d.vm[j]);
-        const float vbar = fmaf(n_g, mv, svj * (float)d.vz[j]);  // s_v sum v' + n m_v
+        const float mv = lo_half(vmr[j]), svj = hi_half(vmr[j]);
+        uint32_t zj;
+        if constexpr (SB == 1) zj = (vzr[j >> 2] >> (8 * (j & 3))) & 0xFFu;
+        else zj = (vzr[j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
+        const float vbar = fmaf(n_g, mv, svj * (float)zj);  // s_v sum v' + n m_v
 #pragma unroll
         for (int rt = 0; rt < GT; ++rt) {
           v4i acc = v4i{0, 0, 0, 0};
 #pragma unroll
-          for (int sl = 0; sl < TILES; ++sl) acc = mfma_i8(pa[rt][sl], unpack16<BITS>(d.vc + j * VW + sl * SW), acc);
-          // Eq. 4: s_p s_v D~ + (s_p sum p~') m_v + m~_p (s_v sum v' + n m_v)
+          for (int sl = 0; sl < TILES; ++sl) acc = mfma_i8(pa[rt][sl], unpack16<BITS>(vcr + j * VW + sl * SW), acc);
+          // Eq. 4: s_p s_v D~ + (s_p sum p~') m_v + m~_p (s_v sum v' + n m_v); the
+          // diagonal s_p against the lane's own s_v gives s_p s_v at (block g, head i)
+          const v4f spv = mfma_f32(pr0[rt], svj, v4f{0.0f, 0.0f, 0.0f, 0.0f});
           o_acc[rt][j] = mfma_f32(pr1[rt], mv, o_acc[rt][j]);
           o_acc[rt][j] = mfma_f32(pr2[rt], vbar, o_acc[rt][j]);
 #pragma unroll
-          for (int i = 0; i < 4; ++i) o_acc[rt][j][i] = fmaf(sp_[rt][i] * svj, (float)acc[i], o_acc[rt][j][i]);
+          for (int i = 0; i < 4; ++i) o_acc[rt][j][i] = fmaf(spv[i], (float)acc[i], o_acc[rt][j][i]);
           if constexpr (MODE == MODE_PV) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               const int gh = rt * 4 + i;
               if (gvalid && gh < G)
                 a.dbg_prod[(((int64_t)s * Hq + hkv * G + gh) * (a.max_len / PI) + vkb) * D + 8 * col + j] =
-                    acc[i] + 128 * (int)d.vz[j];
+                    acc[i] + 128 * (int)zj;
             }
           }
         }
@@ -648,25 +734,11 @@ __global__ __launch_bounds__(256, HACK_DECODE_WAVES_PER_SIMD) void decode_kernel
     __builtin_amdgcn_wave_barrier();
   };
   int si = wave;
-#if HACK_DECODE_PREFETCH
-  if (si < nspan_full) {
-    SpanData<BITS, PI> cur;
-    load_span(cur, t0 + si * SPAN, std::false_type{});
-    for (; si < nspan_full; si += kWaves) {
-      SpanData<BITS, PI> nxt;
-      const bool more = si + kWaves < nspan_full;
-      if (more) load_span(nxt, t0 + (si + kWaves) * SPAN, std::false_type{});
-      compute_span(cur, t0 + si * SPAN, std::false_type{});
-      if (more) cur = nxt;
-    }
-  }
-#else
   for (; si < nspan_full; si += kWaves) {
     SpanData<BITS, PI> cur;
     load_span(cur, t0 + si * SPAN, std::false_type{});
     compute_span(cur, t0 + si * SPAN, std::false_type{});
   }
-#endif
   if (nspan - 1 >= nspan_full && (nspan - 1) % kWaves == wave) {
     SpanData<BITS, PI> last;
     load_span(last, t0 + (nspan - 1) * SPAN, std::true_type{});
@@ -679,20 +751,10 @@ __global__ __launch_bounds__(256, HACK_DECODE_WAVES_PER_SIMD) void decode_kernel
   for (int rt = 0; rt < GT; ++rt) {
     float ov[8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      float v4[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        float v = o_acc[rt][j][i];
-        v += __shfl_xor(v, 16, 64);
-        v += __shfl_xor(v, 32, 64);
-        v4[i] = v;
-      }
-      ov[j] = pick4(v4, grp);
-    }
+    for (int j = 0; j < 8; ++j) ov[j] = reduce_scatter4(o_acc[rt][j][0], o_acc[rt][j][1], o_acc[rt][j][2], o_acc[rt][j][3]);
     const float lsum = row16_sum(l_run[rt]);
     // lane group g writes head slot 4*rt + g: channels 8*col .. 8*col+7
-    float* dst = &mrg_o[wave][rt * 4 + grp][8 * col];
+    float* dst = &wl.mrg_o[rt * 4 + grp][8 * col];
 #pragma unroll
     for (int j = 0; j < 8; ++j) dst[j] = ov[j];
     if (col == 0) {
@@ -717,8 +779,8 @@ __global__ __launch_bounds__(256, HACK_DECODE_WAVES_PER_SIMD) void decode_kernel
       if (mrg_ml[w][gh][1] > 0.0f) {
         const float wt = MODE == MODE_PV ? 1.0f : __builtin_amdgcn_exp2f(mrg_ml[w][gh][0] - mmax);
         lsum = fmaf(mrg_ml[w][gh][1], wt, lsum);
-        o0 = fmaf(mrg_o[w][gh][ch], wt, o0);
-        o1 = fmaf(mrg_o[w][gh][ch + 1], wt, o1);
+        o0 = fmaf(wl_all[w].mrg_o[gh][ch], wt, o0);
+        o1 = fmaf(wl_all[w].mrg_o[gh][ch + 1], wt, o1);
       }
     }
     float* o = a.out + ((int64_t)s * Hq + hkv * G + gh) * D + ch;
@@ -745,30 +807,51 @@ __global__ __launch_bounds__(256, HACK_DECODE_WAVES_PER_SIMD) void decode_kernel
 // (max, sum, O) of its chunks.  Runs as a separate launch so that the partials
 // written by other workgroups are visible without device-wide cache flushes.
 __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeArgs a) {
-  constexpr int D = 128, REC = 4 + D;
+  constexpr int D = 128, REC = 4 + D, U = 8;
   const int s = blockIdx.y, hkv = blockIdx.x;
   const int G = a.group, Hq = a.num_q_heads;
   const int L = max(0, min(a.lens[s], a.max_len));
   const int nsplit = (L + a.chunk - 1) / a.chunk;
   if (nsplit <= 1) return;  // written directly by the attention kernel
   const int64_t pair = (int64_t)s * a.c.kv_heads + hkv;
-  // thread (head gh, channels 4*q .. 4*q+3), one pass with a running max
+  // thread (head gh, channels 4*q .. 4*q+3), one pass with a running max over
+  // groups of U chunks whose loads are all issued before any of them is used
   for (int idx = threadIdx.x; idx < G * (D / 4); idx += blockDim.x) {
     const int gh = idx / (D / 4), ch = 4 * (idx % (D / 4));
     float mrun = -INFINITY, lsum = 0.0f;
     float4 o = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll 4
-    for (int sp = 0; sp < nsplit; ++sp) {
-      const float* rec = a.partials + ((pair * a.splits + sp) * G + gh) * REC;
-      const float ms = rec[0], ls = rec[1];
-      const float4 os = *reinterpret_cast<const float4*>(rec + 4 + ch);
-      const float mn = fmaxf(mrun, ms);
-      const float wa = __builtin_amdgcn_exp2f(mrun - mn), wb = __builtin_amdgcn_exp2f(ms - mn);
-      lsum = lsum * wa + ls * wb;
-      o.x = o.x * wa + os.x * wb;
-      o.y = o.y * wa + os.y * wb;
-      o.z = o.z * wa + os.z * wb;
-      o.w = o.w * wa + os.w * wb;
+    for (int sp0 = 0; sp0 < nsplit; sp0 += U) {
+      float ms[U], ls[U];
+      float4 os[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        if (sp0 + u < nsplit) {
+          const float* rec = a.partials + ((pair * a.splits + sp0 + u) * G + gh) * REC;
+          const float2 ml = *reinterpret_cast<const float2*>(rec);
+          ms[u] = ml.x;
+          ls[u] = ml.y;
+          os[u] = *reinterpret_cast<const float4*>(rec + 4 + ch);
+        } else {
+          ms[u] = -INFINITY;
+          ls[u] = 0.0f;
+          os[u] = float4{0.0f, 0.0f, 0.0f, 0.0f};
+        }
+      }
+      float mn = mrun;
+#pragma unroll
+      for (int u = 0; u < U; ++u) mn = fmaxf(mn, ms[u]);
+      const float wa = __builtin_amdgcn_exp2f(mrun - mn);
+      lsum *= wa;
+      o.x *= wa; o.y *= wa; o.z *= wa; o.w *= wa;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const float wb = ls[u] > 0.0f ? __builtin_amdgcn_exp2f(ms[u] - mn) : 0.0f;
+        lsum = fmaf(ls[u], wb, lsum);
+        o.x = fmaf(os[u].x, wb, o.x);
+        o.y = fmaf(os[u].y, wb, o.y);
+        o.z = fmaf(os[u].z, wb, o.z);
+        o.w = fmaf(os[u].w, wb, o.w);
+      }
       mrun = mn;
     }
     const float inv = 1.0f / lsum;
@@ -777,18 +860,25 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeArgs a) {
   }
 }
 
+static int occupancy_of(const hack_kv_layout& lay, int G) {
+  const int gt = G <= 4 ? 1 : 2;
+  if (lay.kv_bits == 2 && lay.partition == 32 && gt == 1) return decode_occupancy<2, 32, 1>();
+  return 2;
+}
+
 DecodePlan plan_decode(const hack_kv_layout& lay, int batch, int num_q_heads, int max_len) {
   DecodePlan p{};
-  const int64_t wg_tokens = 4 * lay.partition * kWaves;  // one span per wave
+  const int64_t span = 4 * lay.partition;
   const int64_t pairs = (int64_t)batch * lay.num_kv_heads;
   const int64_t G = lay.num_kv_heads > 0 ? num_q_heads / lay.num_kv_heads : 0;
-  // workgroups to aim for over the whole grid (four waves each, 256 compute units)
-  const int64_t target = HACK_DECODE_TARGET_WGS;
-  int64_t chunk = pairs > 0 ? ((int64_t)max_len * pairs + target - 1) / target : wg_tokens;
-  chunk = ((chunk + wg_tokens - 1) / wg_tokens) * wg_tokens;
-  if (chunk < wg_tokens) chunk = wg_tokens;
-  p.chunk = (int)chunk;
-  p.splits = max_len > 0 ? (int)(((int64_t)max_len + chunk - 1) / chunk) : 1;
+  // one workgroup per compute unit and resident wave slot of a SIMD
+  const int64_t per_cu = HACK_DECODE_WGS_PER_CU > 0 ? HACK_DECODE_WGS_PER_CU : occupancy_of(lay, (int)G);
+  const int64_t target = kComputeUnits * per_cu;
+  const int64_t spans_seq = ((int64_t)max_len + span - 1) / span;
+  int64_t wg_spans = pairs > 0 ? (spans_seq * pairs + target - 1) / target : 1;
+  if (wg_spans < 1) wg_spans = 1;
+  p.chunk = (int)(wg_spans * span);
+  p.splits = max_len > 0 ? (int)(((int64_t)max_len + p.chunk - 1) / p.chunk) : 1;
   p.partial_floats = pairs * p.splits * G * (4 + lay.head_dim);
   p.workspace_bytes = ((p.partial_floats * 4 + 255) / 256) * 256;
   return p;
