@@ -806,26 +806,26 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
 // Split-K merge: one workgroup per (sequence, kv head) combines the partial
 // (max, sum, O) of its chunks.  Runs as a separate launch so that the partials
 // written by other workgroups are visible without device-wide cache flushes.
+// The records of all planned chunks are read together with the length (records
+// of chunks past the sequence are stale and masked out afterwards), so the
+// kernel waits on memory once per group of U chunks.
 __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeArgs a) {
   constexpr int D = 128, REC = 4 + D, U = 8;
   const int s = blockIdx.y, hkv = blockIdx.x;
   const int G = a.group, Hq = a.num_q_heads;
-  const int L = max(0, min(a.lens[s], a.max_len));
-  const int nsplit = (L + a.chunk - 1) / a.chunk;
-  if (nsplit <= 1) return;  // written directly by the attention kernel
   const int64_t pair = (int64_t)s * a.c.kv_heads + hkv;
-  // thread (head gh, channels 4*q .. 4*q+3), one pass with a running max over
-  // groups of U chunks whose loads are all issued before any of them is used
+  const int Lraw = a.lens[s];
+  // thread (head gh, channels 4*q .. 4*q+3), one pass with a running max
   for (int idx = threadIdx.x; idx < G * (D / 4); idx += blockDim.x) {
     const int gh = idx / (D / 4), ch = 4 * (idx % (D / 4));
     float mrun = -INFINITY, lsum = 0.0f;
     float4 o = {0.0f, 0.0f, 0.0f, 0.0f};
-    for (int sp0 = 0; sp0 < nsplit; sp0 += U) {
+    for (int sp0 = 0; sp0 < a.splits; sp0 += U) {
       float ms[U], ls[U];
       float4 os[U];
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        if (sp0 + u < nsplit) {
+        if (sp0 + u < a.splits) {
           const float* rec = a.partials + ((pair * a.splits + sp0 + u) * G + gh) * REC;
           const float2 ml = *reinterpret_cast<const float2*>(rec);
           ms[u] = ml.x;
@@ -837,15 +837,19 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeArgs a) {
           os[u] = float4{0.0f, 0.0f, 0.0f, 0.0f};
         }
       }
+      const int L = max(0, min(Lraw, a.max_len));
+      const int nsplit = (L + a.chunk - 1) / a.chunk;
+      if (nsplit <= 1) return;  // written directly by the attention kernel
       float mn = mrun;
 #pragma unroll
-      for (int u = 0; u < U; ++u) mn = fmaxf(mn, ms[u]);
-      const float wa = __builtin_amdgcn_exp2f(mrun - mn);
+      for (int u = 0; u < U; ++u)
+        if (sp0 + u < nsplit && ls[u] > 0.0f) mn = fmaxf(mn, ms[u]);
+      const float wa = mrun == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(mrun - mn);
       lsum *= wa;
       o.x *= wa; o.y *= wa; o.z *= wa; o.w *= wa;
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        const float wb = ls[u] > 0.0f ? __builtin_amdgcn_exp2f(ms[u] - mn) : 0.0f;
+        const float wb = (sp0 + u < nsplit && ls[u] > 0.0f) ? __builtin_amdgcn_exp2f(ms[u] - mn) : 0.0f;
         lsum = fmaf(ls[u], wb, lsum);
         o.x = fmaf(os[u].x, wb, o.x);
         o.y = fmaf(os[u].y, wb, o.y);
