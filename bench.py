@@ -49,6 +49,24 @@ def append_bytes(B: int, H: int, d: int, bits: int, pi: int, sum_bytes: int, T_a
     return B * H * per
 
 
+def profiled_traffic(kernel_file: str, summary: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or None when
+    the kernel source has changed since the counters were taken."""
+    import hashlib
+    try:
+        text = open(os.path.join(ROOT, "profiles", summary)).read()
+        src = open(os.path.join(ROOT, "paper_2502_03589_amd", "csrc", kernel_file), "rb").read()
+    except OSError:
+        return None
+    fields = dict(line.split(": ", 1) for line in text.splitlines() if ": " in line and not line.startswith(" "))
+    if fields.get("kernel_source_sha256", "").strip() != hashlib.sha256(src).hexdigest():
+        return None
+    try:
+        return int(fields["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -214,9 +232,10 @@ def main():
                    "head_dim": d, "context": L0, "kv_bits": bits, "partition": pi, "qp_bits": 8,
                    "outlier_k_channels": wl.outlier_channels, "cache_replicas": R,
                    "step": "append 1 token + decode attention", "parallelism": "1 GPU"},
-        "roofline": {"bound": "hbm", "kernel": "decode_kernel", "achieved": round(achieved, 2),
+        "roofline": {"bound": "hbm", "kernel": "hack_attend_decode (decode_kernel + decode_merge_kernel)", "achieved": round(achieved, 2),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": None, "avg_kernel_us": round(avg_kern_ms * 1e3, 3),
+                     "traffic": profiled_traffic("kernels_decode.hip", "decode_llama8b_l4096_hbm_counters.txt"),
+                     "avg_kernel_us": round(avg_kern_ms * 1e3, 3),
                      "bytes_per_launch": int(np.mean(dec_bytes))},
     }
     if not args.no_prefill and args.only is None:
