@@ -76,6 +76,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prefill", action="store_true")
     ap.add_argument("--prefill-iters", type=int, default=10)
+    ap.add_argument("--workload", choices=["decode_70b_ragged", "decode_long_l131072"], default=None,
+                    help="time another decode workload instead (one JSON line per configuration; "
+                         "not the headline line)")
     ap.add_argument("--only", choices=["decode", "prefill", "copy"], default=None,
                     help="profiling aid: run one leg alone (copy = plain device copy of a known size, "
                          "the calibration for HBM byte counters)")
@@ -129,6 +132,9 @@ def main():
         sys.exit(2)
     if args.only == "copy":
         copy_calibration()
+        return
+    if args.workload is not None:
+        bench_workload(args.workload, args.steps, args.warmup)
         return
     if args.only == "prefill":
         print(json.dumps({"prefill": bench_prefill(args.prefill_iters)}), flush=True)
@@ -285,6 +291,87 @@ def bench_prefill(iters: int):
     return {"workload": "prefill_l8192", "int8_ops": ops, "attend_ms": round(a_ms, 4),
             "quantize_ms": round(float(np.median(qt)), 4), "TOPS": round(tops, 2),
             "peak_TOPS": INT8_PEAK_TOPS, "frac": round(tops / INT8_PEAK_TOPS, 4)}
+
+
+def bench_workload(name: str, steps: int, warmup: int):
+    """Decode throughput on the ragged paged workload (decode calls only) or on the
+    128K-context loop (append + decode per step, 2/4 bits, both open-block modes)."""
+    import torch
+    from paper_2502_03589_amd import hack as hk
+    from paper_2502_03589_amd import synth
+    dev = torch.device("cuda:0")
+    wl = synth.WORKLOADS[name]
+    B, Hq, H, d, pi = wl.batch, wl.q_heads, wl.kv_heads, wl.head_dim, wl.partition
+
+    def timed(fn, n):
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+        for i in range(n):
+            ev[i][0].record()
+            fn(i)
+            ev[i][1].record()
+        torch.cuda.synchronize()
+        return float(np.mean([a.elapsed_time(b) for a, b in ev]))
+
+    if name == "decode_70b_ragged":
+        lens = synth.uniform_lengths(wl.seed, B, *wl.len_range)
+        table, pages = synth.page_table(wl.seed, lens, wl.page_tokens)
+        lay = hk.hack_kv_layout_make(d, H, wl.kv_bits, pi, wl.page_tokens)
+        cache = hk.KVCache(lay, pages, B, torch.from_numpy(table).to(dev), dev)
+        lens_dev = torch.from_numpy(lens.copy()).to(dev)
+        for b in range(B):
+            L = int(lens[b])
+            k = torch.from_numpy(synth.normal_f16(wl.seed, "k", (1, H, L, d), sub=1 + b)).to(dev)
+            v = torch.from_numpy(synth.normal_f16(wl.seed, "v", (1, H, L, d), sub=1 + b)).to(dev)
+            hk.hack_quantize(lay, cache.sequences(b, 1), k, v, lens_dev[b:b + 1], L)
+        q = torch.from_numpy(synth.normal_f16(wl.seed, "q", (B, Hq, d))).to(dev)
+        ws = hk.decode_workspace(lay, B, Hq, int(lens.max()))
+        out = torch.empty((B, Hq, d), dtype=torch.float32, device=dev)
+        call = hk.bind_attend_decode(lay, cache, q, lens_dev, int(lens.max()), hk.TAIL_FP16, out, ws)
+        for _ in range(warmup):
+            call()
+        ms = timed(lambda i: call(), steps)
+        sb = lay.sum_bytes
+        nbytes = sum(H * decode_bytes_per_seq_head(int(L), d, wl.kv_bits, pi, sb) for L in lens) + B * Hq * d * 6
+        print(json.dumps({"workload": name, "metric": "decode GB/s", "value": round(nbytes / ms / 1e6, 2),
+                          "unit": "GB/s", "us_per_call": round(ms * 1e3, 2), "bytes_per_call": int(nbytes),
+                          "frac_of_8TBs": round(nbytes / ms / 1e6 / HBM_PEAK_GBS, 4), "tokens": int(lens.sum())}),
+              flush=True)
+        return
+    # decode_long_l131072: 64 steps of (append one token, decode) after quantizing 131072 tokens
+    L0, nsteps = wl.context, wl.steps
+    cap = L0 + nsteps
+    k_all = torch.from_numpy(np.stack([synth.normal_f16(wl.seed, "k", (H, cap, d), sub=1 + b) for b in range(B)])).to(dev)
+    v_all = torch.from_numpy(np.stack([synth.normal_f16(wl.seed, "v", (H, cap, d), sub=1 + b) for b in range(B)])).to(dev)
+    qs = torch.from_numpy(np.stack([synth.normal_f16(wl.seed, "q", (B, Hq, d), sub=1 + i) for i in range(nsteps)])).to(dev)
+    knew = [k_all[:, :, L0 + i].contiguous() for i in range(nsteps)]
+    vnew = [v_all[:, :, L0 + i].contiguous() for i in range(nsteps)]
+    for bits in (2, 4):
+        for tail in (hk.TAIL_FP16, hk.TAIL_REQUANT):
+            lay = hk.hack_kv_layout_make(d, H, bits, pi, cap)
+            cache = hk.KVCache(lay, B, B, None, dev)
+            lens = torch.full((B,), L0, dtype=torch.int32, device=dev)
+            hk.hack_quantize(lay, cache, k_all[:, :, :L0].contiguous(), v_all[:, :, :L0].contiguous(), lens, L0)
+            ws = hk.decode_workspace(lay, B, Hq, cap)
+            out = torch.empty((B, Hq, d), dtype=torch.float32, device=dev)
+            app = [hk.bind_append(lay, cache, knew[i], vnew[i], lens, cap - 1, tail) for i in range(nsteps)]
+            dec = [hk.bind_attend_decode(lay, cache, qs[i], lens, cap, tail, out, ws) for i in range(nsteps)]
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for i in range(nsteps):
+                app[i]()
+                dec[i]()
+            torch.cuda.synchronize()
+            step_ms = (time.perf_counter() - t0) * 1e3 / nsteps
+            sb = lay.sum_bytes
+            dbytes = np.mean([B * H * decode_bytes_per_seq_head(L0 + i + 1, d, bits, pi, sb) for i in range(nsteps)])
+            dbytes += B * Hq * d * 6
+            abytes = np.mean([append_bytes(B, H, d, bits, pi, sb, (L0 + i + 1) % pi) for i in range(nsteps)])
+            print(json.dumps({"workload": name, "kv_bits": bits, "tail_mode": "requant" if tail else "fp16",
+                              "metric": "append+decode GB/s", "value": round((dbytes + abytes) / step_ms / 1e6, 2),
+                              "unit": "GB/s", "ms_per_step": round(step_ms, 4), "decode_bytes": int(dbytes),
+                              "frac_of_8TBs": round((dbytes + abytes) / step_ms / 1e6 / HBM_PEAK_GBS, 4)}),
+                  flush=True)
+            del cache, ws
 
 
 if __name__ == "__main__":

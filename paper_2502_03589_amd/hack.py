@@ -152,6 +152,34 @@ class KVCache:
     def nbytes(self) -> int:
         return sum(b.numel() for b in self.buffers.values())
 
+    def sequences(self, first: int, count: int) -> "CacheSlice":
+        """A view of sequences [first, first + count) of this cache, for calls that
+        take a smaller batch (e.g. quantizing one long sequence at a time)."""
+        return CacheSlice(self, first, count)
+
+
+class CacheSlice:
+    """Sequences [first, first + count) of a KVCache: the same buffers, with the
+    per-sequence pointers (block-table rows, open-block rows, and for a contiguous
+    cache the pages themselves) advanced to `first`."""
+
+    def __init__(self, cache: KVCache, first: int, count: int):
+        if first < 0 or count < 0 or first + count > cache.num_seqs:
+            raise ValueError("sequence range outside the cache")
+        lay, src = cache.layout, cache.struct
+        c = hack_kv_cache()
+        for name, _ in hack_kv_cache._fields_:
+            setattr(c, name, getattr(src, name))
+        if cache.block_table is None:
+            for i, name in enumerate(SECTIONS):
+                if i != V_TAIL:
+                    setattr(c, name, getattr(src, name) + first * hack_kv_bytes(lay, 1, i))
+            c.num_pages = count
+        else:
+            c.block_table_dev = src.block_table_dev + first * src.max_blocks_per_seq * 4
+        c.v_tail = src.v_tail + first * hack_kv_bytes(lay, 1, V_TAIL)
+        self.layout, self.struct, self.parent = lay, c, cache
+
 
 def hack_quantize(layout, cache: KVCache, k: torch.Tensor, v: torch.Tensor, seq_lens: torch.Tensor,
                   max_len: Optional[int] = None, stream=None):
