@@ -11,7 +11,13 @@
 //   S^T = K'Q'^T  v_mfma_i32_16x16{32,64}_i8, one per (16-token tile, 16-row tile,
 //            K partition): A = K codes (lane = token), B = 8-bit Q codes minus 128
 //            quantized in registers (lane = query row).  Lane (row n, group g) gets
-//            tokens 4g..4g+3 of the tile for row n; Eq. 4 with cached K sums on VALU.
+//            tokens 4g..4g+3 of the tile for row n.  Eq. 4: the rank-1 terms
+//            (m~_q s_k sum k' + R m_k, all partitions) are outer products of a
+//            token-side and a row-side vector, so one v_mfma_f32_16x16x4_f32 per
+//            tile forms them in the tile's layout; the VALU applies s_q s_k to each
+//            converted integer product.  (Moving the scale products or the P'V'
+//            rank-1 terms onto f32 MFMAs too was measured slower: a 16x16x4 f32
+//            MFMA costs more matrix-core time than the VALU work it replaces.)
 //   softmax  online per row with a lazily raised reference max; causal mask.
 //   P        8-bit per (row, V block) with round-to-nearest-even codes; the masked
 //            zeros inside the diagonal block are quantized with it.  The lane's codes
@@ -24,12 +30,23 @@
 namespace hack {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
+typedef float v4f __attribute__((ext_vector_type(4)));
 
 namespace {
 
 constexpr int kRows = 32;        // query rows per workgroup (two 16-row MFMA tiles)
 constexpr float kScale = 0.12751743074941640f;  // log2(e) / sqrt(128)
 constexpr float kSlack = 8.0f;   // reference max raised only beyond this (log2 units)
+
+#ifndef HACK_PREFILL_SCALE_MFMA
+#define HACK_PREFILL_SCALE_MFMA 0  // s_q s_k and s_p s_v as outer-product MFMAs (else VALU)
+#endif
+#ifndef HACK_PREFILL_QK_RANK_MFMA
+#define HACK_PREFILL_QK_RANK_MFMA 1  // Q'K' rank-1 terms as outer-product MFMAs (else VALU)
+#endif
+#ifndef HACK_PREFILL_PV_RANK_MFMA
+#define HACK_PREFILL_PV_RANK_MFMA 0  // P'V' rank-1 terms as outer-product MFMAs (else VALU)
+#endif
 
 template <int PI>
 struct PrefillCfg {
@@ -80,6 +97,10 @@ struct Stage {
   float km[PrefillCfg<PI>::P][3][PI];          // per token and partition: s_k, s_k*sum k', m_k
   float vm[3][128];                            // per channel: s_v, m_v, s_v*sum v' + PI*m_v
 };
+
+__device__ __forceinline__ v4f mfma_f32(float a, float b, v4f c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
 
 // Max / min / sum over the four lane groups (lanes l, l^16, l^32, l^48).
 __device__ __forceinline__ float xg_max(float x) {
@@ -306,12 +327,22 @@ __global__ __launch_bounds__(512, 1) void prefill_kernel(PrefillArgs a) {
     }
   }
 
+  // Row-side operands of the outer-product MFMAs (lane (row, group g) supplies slot g):
+  // rank terms of partitions 2m, 2m+1 as (m~_q, R, m~_q, R); the scale s_q in slot 0.
+  float brank[(P + 1) / 2], bscale[P];
+#pragma unroll
+  for (int m = 0; m < (P + 1) / 2; ++m) {
+    const int p = min(P - 1, 2 * m + (grp >> 1));
+    const bool live = 2 * m + (grp >> 1) < P;
+    brank[m] = live ? ((grp & 1) ? rq[p] : mq[p]) : 0.0f;
+  }
+#pragma unroll
+  for (int p = 0; p < P; ++p) bscale[p] = grp == 0 ? sq[p] : 0.0f;
+
   float m_ref = -INFINITY, l_run = 0.0f;
-  float o[8][4];
+  v4f o[8];
 #pragma unroll
-  for (int j = 0; j < 8; ++j)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) o[j][i] = 0.0f;
+  for (int j = 0; j < 8; ++j) o[j] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
 
   StageRegs<BITS, PI> sr;
   if (nblk > 0) {
@@ -328,33 +359,59 @@ __global__ __launch_bounds__(512, 1) void prefill_kernel(PrefillArgs a) {
     const int tb0 = kb * PI;
 
     // ---------------- S^T tiles and Eq. 4 (lane: row `row`, tokens 16 tl + 4 grp + i) ----------------
+    // masking is needed only in the block holding the length or this wave's diagonal
+    const bool need_mask = tb0 + PI > L || (a.causal && tb0 + PI - 1 > r0 + 16 * (wave >> 2));
     float sv[TL][4];
 #pragma unroll
     for (int tl = 0; tl < TL; ++tl) {
-      float acc_s[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+      const int tt = 16 * tl + col;  // token of this lane's A-operand row
+      // rank-1 terms summed over the partitions: token-side slot g = (partition, term)
+      v4f s4 = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+#if HACK_PREFILL_QK_RANK_MFMA
+#pragma unroll
+      for (int m = 0; m < (P + 1) / 2; ++m) {
+        const int p = min(P - 1, 2 * m + (grp >> 1));
+        const bool live = 2 * m + (grp >> 1) < P;
+        const float ak = live ? st.km[p][1 + (grp & 1)][tt] : 0.0f;  // s_k sum k' | m_k
+        s4 = mfma_f32(ak, brank[m], s4);
+      }
+#else
 #pragma unroll
       for (int p = 0; p < P; ++p) {
-        const opT ka = OP::lds(&st.k[16 * tl + col][p * PI + grp * KSL]);
-        const v4i acc = OP::mfma(ka, qop[p], v4i{0, 0, 0, 0});
-        const float4 f0 = *reinterpret_cast<const float4*>(&st.km[p][0][16 * tl + 4 * grp]);
         const float4 f1 = *reinterpret_cast<const float4*>(&st.km[p][1][16 * tl + 4 * grp]);
         const float4 f2 = *reinterpret_cast<const float4*>(&st.km[p][2][16 * tl + 4 * grp]);
-        const float ksk[4] = {f0.x, f0.y, f0.z, f0.w};
         const float kak[4] = {f1.x, f1.y, f1.z, f1.w};
         const float kmk[4] = {f2.x, f2.y, f2.z, f2.w};
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          // s_q s_k C~ + m~_q (s_k sum k') + R m_k
-          float x = fmaf(sq[p] * ksk[i], (float)acc[i], acc_s[i]);
-          x = fmaf(mq[p], kak[i], x);
-          acc_s[i] = fmaf(rq[p], kmk[i], x);
-        }
+        for (int i = 0; i < 4; ++i) s4[i] = fmaf(rq[p], kmk[i], fmaf(mq[p], kak[i], s4[i]));
       }
+#endif
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int tok = tb0 + 16 * tl + 4 * grp + i;
-        const bool masked = tok >= L || (a.causal && tok > row);
-        sv[tl][i] = masked ? -INFINITY : acc_s[i];
+      for (int p = 0; p < P; ++p) {
+        const opT ka = OP::lds(&st.k[tt][p * PI + grp * KSL]);
+        const v4i acc = OP::mfma(ka, qop[p], v4i{0, 0, 0, 0});
+#if HACK_PREFILL_SCALE_MFMA
+        const float ask = grp == 0 ? st.km[p][0][tt] : 0.0f;  // s_k
+        const v4f sqk = mfma_f32(ask, bscale[p], v4f{0.0f, 0.0f, 0.0f, 0.0f});
+#pragma unroll
+        for (int i = 0; i < 4; ++i) s4[i] = fmaf(sqk[i], (float)acc[i], s4[i]);  // s_q s_k C~
+#else
+        const float4 fk = *reinterpret_cast<const float4*>(&st.km[p][0][16 * tl + 4 * grp]);
+        const float ksk[4] = {fk.x, fk.y, fk.z, fk.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) s4[i] = fmaf(sq[p] * ksk[i], (float)acc[i], s4[i]);  // s_q s_k C~
+#endif
+      }
+      if (need_mask) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int tok = tb0 + 16 * tl + 4 * grp + i;
+          const bool masked = tok >= L || (a.causal && tok > row);
+          sv[tl][i] = masked ? -INFINITY : s4[i];
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) sv[tl][i] = s4[i];
       }
     }
 
@@ -369,9 +426,7 @@ __global__ __launch_bounds__(512, 1) void prefill_kernel(PrefillArgs a) {
       const float alpha = __builtin_amdgcn_exp2f(m_ref - bmax);
       l_run *= alpha;
 #pragma unroll
-      for (int j = 0; j < 8; ++j)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) o[j][i] *= alpha;
+      for (int j = 0; j < 8; ++j) o[j] *= alpha;
       m_ref = bmax;
     }
     float pt[TL][4];
@@ -406,25 +461,41 @@ __global__ __launch_bounds__(512, 1) void prefill_kernel(PrefillArgs a) {
       // sum of the signed codes of this row's block: all-ones A operand
       const v4i z = OP::mfma(OP::ones(), pop, v4i{0, 0, 0, 0});
       const float pz = ps * (float)z[0];       // s_p * sum p~'
+      // row-side operands: rank terms (s_p sum p~', m~_p) in slots 0, 1; s_p in slot 0
+      const float bpr = grp == 0 ? pz : (grp == 1 ? pm : 0.0f);
+      const float bps = grp == 0 ? ps : 0.0f;
 
       // ---------------- O^T += V'^T P'^T with Eq. 4 (lane: row, channels 16 j + 4 grp + i) ----------------
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        const opT va = OP::lds(&st.v[16 * j + col][grp * KSL]);
+        const int cc = 16 * j + col;  // channel of this lane's A-operand row
+        const opT va = OP::lds(&st.v[cc][grp * KSL]);
         const v4i acc = OP::mfma(va, pop, v4i{0, 0, 0, 0});
-        const float4 fs = *reinterpret_cast<const float4*>(&st.vm[0][16 * j + 4 * grp]);
-        const float4 fm = *reinterpret_cast<const float4*>(&st.vm[1][16 * j + 4 * grp]);
-        const float4 fb = *reinterpret_cast<const float4*>(&st.vm[2][16 * j + 4 * grp]);
-        const float vs[4] = {fs.x, fs.y, fs.z, fs.w};
-        const float vmn[4] = {fm.x, fm.y, fm.z, fm.w};
-        const float vbar[4] = {fb.x, fb.y, fb.z, fb.w};
+        // (s_p sum p~') m_v + m~_p (s_v sum v' + n m_v), then s_p s_v D~
+#if HACK_PREFILL_PV_RANK_MFMA
+        const float avr = grp == 0 ? st.vm[1][cc] : (grp == 1 ? st.vm[2][cc] : 0.0f);
+        o[j] = mfma_f32(avr, bpr, o[j]);
+#else
+        {
+          const float4 fm = *reinterpret_cast<const float4*>(&st.vm[1][16 * j + 4 * grp]);
+          const float4 fb = *reinterpret_cast<const float4*>(&st.vm[2][16 * j + 4 * grp]);
+          const float vmn[4] = {fm.x, fm.y, fm.z, fm.w};
+          const float vbar[4] = {fb.x, fb.y, fb.z, fb.w};
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          // s_p s_v D~ + (s_p sum p~') m_v + m~_p (s_v sum v' + n m_v)
-          float x = fmaf(ps * vs[i], (float)acc[i], o[j][i]);
-          x = fmaf(pz, vmn[i], x);
-          o[j][i] = fmaf(pm, vbar[i], x);
+          for (int i = 0; i < 4; ++i) o[j][i] = fmaf(pm, vbar[i], fmaf(pz, vmn[i], o[j][i]));
         }
+#endif
+#if HACK_PREFILL_SCALE_MFMA
+        const float avs = grp == 0 ? st.vm[0][cc] : 0.0f;
+        const v4f spv = mfma_f32(avs, bps, v4f{0.0f, 0.0f, 0.0f, 0.0f});
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[j][i] = fmaf(spv[i], (float)acc[i], o[j][i]);
+#else
+        const float4 fs = *reinterpret_cast<const float4*>(&st.vm[0][16 * j + 4 * grp]);
+        const float vs[4] = {fs.x, fs.y, fs.z, fs.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[j][i] = fmaf(ps * vs[i], (float)acc[i], o[j][i]);
+#endif
       }
     } else {
       // fp16 open block: O[row][ch] += sum_{t < T} p[row][t] v_t[ch] with unquantized p
