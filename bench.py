@@ -238,7 +238,7 @@ def main():
                    "head_dim": d, "context": L0, "kv_bits": bits, "partition": pi, "qp_bits": 8,
                    "outlier_k_channels": wl.outlier_channels, "cache_replicas": R,
                    "step": "append 1 token + decode attention", "parallelism": "1 GPU"},
-        "roofline": {"bound": "hbm", "kernel": "hack_attend_decode (decode_kernel + decode_merge_kernel)", "achieved": round(achieved, 2),
+        "roofline": {"bound": "hbm", "kernel": "decode_kernel (hack_attend_decode, split-K merge fused)", "achieved": round(achieved, 2),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": profiled_traffic("kernels_decode.hip", "decode_llama8b_l4096_hbm_counters.txt"),
                      "avg_kernel_us": round(avg_kern_ms * 1e3, 3),

@@ -147,7 +147,8 @@ hack_status hack_append(const hack_kv_layout* layout, const hack_kv_cache* cache
                         int32_t batch, int32_t max_len, int32_t tail_mode, hipStream_t stream);
 
 /* Workspace bytes hack_attend_decode needs for these sizes (the split-K partial
- * results: max, sum and unnormalized O per chunk and query head).  -1 on invalid
+ * results: max, sum and unnormalized O per chunk and query head, and one counter per
+ * (sequence, kv head)).  -1 on invalid
  * arguments. */
 int64_t hack_decode_workspace_bytes(const hack_kv_layout* layout, int32_t batch,
                                     int32_t num_q_heads, int32_t max_len);
@@ -157,9 +158,11 @@ int64_t hack_decode_workspace_bytes(const hack_kv_layout* layout, int32_t batch,
  * attends kv head h / (H_q/H_kv).  Per sequence, all seq_lens[s] cached tokens are
  * attended (0 <= seq_lens[s] <= max_len; a sequence of length 0 yields zeros).
  * out_dev: fp32 [batch][H_q][head_dim].  workspace_dev must hold
- * hack_decode_workspace_bytes(...) bytes (no initialization needed) and must not
- * be shared by calls that may run concurrently.  One or two kernels are launched
- * (the second merges the chunks of long sequences).
+ * hack_decode_workspace_bytes(...) bytes, must be zero-filled before its first use
+ * (every call leaves it that way: it holds per-sequence chunk counters next to the
+ * chunk records) and must not be shared by calls that may run concurrently.  One
+ * kernel is launched; when a sequence is split into several chunks, the workgroup
+ * that finishes its last chunk merges them.
  * Requires head_dim 128, partition 32 or 64, H_q/H_kv <= 8 and, for a paged cache,
  * page_tokens a multiple of 4 * partition (else HACK_ERR_UNSUPPORTED). */
 hack_status hack_attend_decode(const hack_kv_layout* layout, const hack_kv_cache* cache,

@@ -186,6 +186,7 @@ hack_status hack_attend_decode(const hack_kv_layout* layout, const hack_kv_cache
   if (batch == 0) return HACK_OK;
   a.out = out_dev;
   a.partials = static_cast<float*>(workspace_dev);
+  a.counters = reinterpret_cast<int32_t*>(static_cast<uint8_t*>(workspace_dev) + plan.counter_offset);
   a.chunk = plan.chunk;
   a.splits = plan.splits;
   a.tail_requant = tail_mode == HACK_TAIL_REQUANT;

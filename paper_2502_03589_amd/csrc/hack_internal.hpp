@@ -17,6 +17,7 @@ struct DecodePlan {
   int chunk;
   int splits;
   int64_t partial_floats;   // batch * H_kv * splits * G * (4 + head_dim)
+  int64_t counter_offset;   // byte offset of the per-(sequence, kv head) counters
   int64_t workspace_bytes;
 };
 
@@ -38,6 +39,7 @@ struct DecodeArgs {
   const int32_t* lens;    // [B]
   float* out;             // [B][H_q][128]
   float* partials;        // [B][H_kv][splits][G][4 + 128]: max, sum, pad, O
+  int32_t* counters;      // [B][H_kv] chunks finished (zero between calls)
   int num_q_heads;
   int group;              // H_q / H_kv
   int chunk;

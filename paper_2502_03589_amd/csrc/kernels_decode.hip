@@ -129,6 +129,10 @@ constexpr int decode_occupancy() {
   return (BITS == 2 && PI == 32 && GT == 1) ? 4 : 2;
 }
 
+#ifndef HACK_DECODE_FUSED_MERGE
+#define HACK_DECODE_FUSED_MERGE 2  // 1/2: the last chunk of a sequence merges (else a second launch)
+#endif
+
 #ifndef HACK_DECODE_WGS_PER_CU
 #define HACK_DECODE_WGS_PER_CU 0  // 0: the kernel's occupancy
 #endif
@@ -228,6 +232,76 @@ __device__ __forceinline__ void lds_dma16(const uint8_t* src, uint8_t* lds) {
 __device__ __forceinline__ void lds_dma4(const uint8_t* src, uint8_t* lds) {
   __builtin_amdgcn_global_load_lds((__attribute__((address_space(1))) const void*)src,
                                    (__attribute__((address_space(3))) void*)lds, 4, 0, 0);
+}
+
+// Split-K merge of one (sequence, kv head): combines the partial (max, sum, O) of
+// its nsplit chunks with a running max and writes O / sum.  The records of all
+// planned chunks are read together (records past the sequence are stale and are
+// masked by the length), so the caller waits on memory once per group of U chunks.
+template <bool COHERENT>
+__device__ __forceinline__ float ld_rec(const float* p) {
+  if constexpr (COHERENT) return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  else return *p;
+}
+
+template <bool COHERENT>
+__device__ __forceinline__ void merge_chunks(const DecodeArgs& a, int s, int hkv, int Lraw) {
+  constexpr int D = 128, REC = 4 + D, U = 8;
+  const int G = a.group, Hq = a.num_q_heads;
+  const int64_t pair = (int64_t)s * a.c.kv_heads + hkv;
+  // thread (head gh, channels 4*q .. 4*q+3)
+  for (int idx = threadIdx.x; idx < G * (D / 4); idx += blockDim.x) {
+    const int gh = idx / (D / 4), ch = 4 * (idx % (D / 4));
+    float mrun = -INFINITY, lsum = 0.0f;
+    float4 o = {0.0f, 0.0f, 0.0f, 0.0f};
+    for (int sp0 = 0; sp0 < a.splits; sp0 += U) {
+      float ms[U], ls[U];
+      float4 os[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        if (sp0 + u < a.splits) {
+          const float* rec = a.partials + ((pair * a.splits + sp0 + u) * G + gh) * REC;
+          if constexpr (COHERENT) {
+            ms[u] = ld_rec<true>(rec);
+            ls[u] = ld_rec<true>(rec + 1);
+            os[u] = float4{ld_rec<true>(rec + 4 + ch), ld_rec<true>(rec + 5 + ch), ld_rec<true>(rec + 6 + ch),
+                           ld_rec<true>(rec + 7 + ch)};
+          } else {
+            const float2 ml = *reinterpret_cast<const float2*>(rec);
+            ms[u] = ml.x;
+            ls[u] = ml.y;
+            os[u] = *reinterpret_cast<const float4*>(rec + 4 + ch);
+          }
+        } else {
+          ms[u] = -INFINITY;
+          ls[u] = 0.0f;
+          os[u] = float4{0.0f, 0.0f, 0.0f, 0.0f};
+        }
+      }
+      const int L = max(0, min(Lraw, a.max_len));
+      const int nsplit = (L + a.chunk - 1) / a.chunk;
+      float mn = mrun;
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (sp0 + u < nsplit && ls[u] > 0.0f) mn = fmaxf(mn, ms[u]);
+      const float wa = mrun == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(mrun - mn);
+      lsum *= wa;
+      o.x *= wa; o.y *= wa; o.z *= wa; o.w *= wa;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const float wb = (sp0 + u < nsplit && ls[u] > 0.0f) ? __builtin_amdgcn_exp2f(ms[u] - mn) : 0.0f;
+        lsum = fmaf(ls[u], wb, lsum);
+        o.x = fmaf(os[u].x, wb, o.x);
+        o.y = fmaf(os[u].y, wb, o.y);
+        o.z = fmaf(os[u].z, wb, o.z);
+        o.w = fmaf(os[u].w, wb, o.w);
+      }
+      mrun = mn;
+    }
+    const float inv = 1.0f / lsum;
+    *reinterpret_cast<float4*>(a.out + ((int64_t)s * Hq + hkv * G + gh) * D + ch) =
+        float4{o.x * inv, o.y * inv, o.z * inv, o.w * inv};
+  }
 }
 
 template <int BITS, int PI, int GT, int MODE>
@@ -793,75 +867,57 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
       o[1] = o1 * inv;
     } else {
       float* rec = a.partials + ((pair * a.splits + split) * G + gh) * REC;
-      if (ch == 0) {
-        rec[0] = mmax;
-        rec[1] = lsum;
+      if constexpr (HACK_DECODE_FUSED_MERGE == 2) {
+        // agent-coherent (write-through) stores: complete at the device's coherence
+        // point once the wave's store counter drains
+        if (ch == 0) {
+          __hip_atomic_store(rec, mmax, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          __hip_atomic_store(rec + 1, lsum, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        __hip_atomic_store(rec + 4 + ch, o0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(rec + 5 + ch, o1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      } else {
+        if (ch == 0) {
+          rec[0] = mmax;
+          rec[1] = lsum;
+        }
+        rec[4 + ch] = o0;
+        rec[5 + ch] = o1;
       }
-      rec[4 + ch] = o0;
-      rec[5 + ch] = o1;
     }
   }
+#if HACK_DECODE_FUSED_MERGE
+  if (MODE == MODE_ATTEND && nsplit > 1) {
+    // The workgroup that finishes a sequence's last chunk merges all of them.
+    __shared__ int last_chunk;
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's record stores are done
+    __syncthreads();
+    if (tid == 0) {
+#if HACK_DECODE_FUSED_MERGE == 2
+      const int done = __hip_atomic_fetch_add(&a.counters[pair], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#else
+      // acquire-release: publishes this chunk's record, and for the last arriver
+      // makes every other chunk's record visible
+      const int done = __hip_atomic_fetch_add(&a.counters[pair], 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+#endif
+      last_chunk = done == nsplit - 1;
+    }
+    __syncthreads();
+    if (last_chunk) {
+      merge_chunks<HACK_DECODE_FUSED_MERGE == 2>(a, s, hkv, a.lens[s]);
+      if (tid == 0) __hip_atomic_store(&a.counters[pair], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+#endif
 }
 
-// Split-K merge: one workgroup per (sequence, kv head) combines the partial
-// (max, sum, O) of its chunks.  Runs as a separate launch so that the partials
-// written by other workgroups are visible without device-wide cache flushes.
-// The records of all planned chunks are read together with the length (records
-// of chunks past the sequence are stale and masked out afterwards), so the
-// kernel waits on memory once per group of U chunks.
+// Split-K merge as a second launch: one workgroup per (sequence, kv head).
 __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeArgs a) {
-  constexpr int D = 128, REC = 4 + D, U = 8;
   const int s = blockIdx.y, hkv = blockIdx.x;
-  const int G = a.group, Hq = a.num_q_heads;
-  const int64_t pair = (int64_t)s * a.c.kv_heads + hkv;
   const int Lraw = a.lens[s];
-  // thread (head gh, channels 4*q .. 4*q+3), one pass with a running max
-  for (int idx = threadIdx.x; idx < G * (D / 4); idx += blockDim.x) {
-    const int gh = idx / (D / 4), ch = 4 * (idx % (D / 4));
-    float mrun = -INFINITY, lsum = 0.0f;
-    float4 o = {0.0f, 0.0f, 0.0f, 0.0f};
-    for (int sp0 = 0; sp0 < a.splits; sp0 += U) {
-      float ms[U], ls[U];
-      float4 os[U];
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        if (sp0 + u < a.splits) {
-          const float* rec = a.partials + ((pair * a.splits + sp0 + u) * G + gh) * REC;
-          const float2 ml = *reinterpret_cast<const float2*>(rec);
-          ms[u] = ml.x;
-          ls[u] = ml.y;
-          os[u] = *reinterpret_cast<const float4*>(rec + 4 + ch);
-        } else {
-          ms[u] = -INFINITY;
-          ls[u] = 0.0f;
-          os[u] = float4{0.0f, 0.0f, 0.0f, 0.0f};
-        }
-      }
-      const int L = max(0, min(Lraw, a.max_len));
-      const int nsplit = (L + a.chunk - 1) / a.chunk;
-      if (nsplit <= 1) return;  // written directly by the attention kernel
-      float mn = mrun;
-#pragma unroll
-      for (int u = 0; u < U; ++u)
-        if (sp0 + u < nsplit && ls[u] > 0.0f) mn = fmaxf(mn, ms[u]);
-      const float wa = mrun == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(mrun - mn);
-      lsum *= wa;
-      o.x *= wa; o.y *= wa; o.z *= wa; o.w *= wa;
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const float wb = (sp0 + u < nsplit && ls[u] > 0.0f) ? __builtin_amdgcn_exp2f(ms[u] - mn) : 0.0f;
-        lsum = fmaf(ls[u], wb, lsum);
-        o.x = fmaf(os[u].x, wb, o.x);
-        o.y = fmaf(os[u].y, wb, o.y);
-        o.z = fmaf(os[u].z, wb, o.z);
-        o.w = fmaf(os[u].w, wb, o.w);
-      }
-      mrun = mn;
-    }
-    const float inv = 1.0f / lsum;
-    *reinterpret_cast<float4*>(a.out + ((int64_t)s * Hq + hkv * G + gh) * D + ch) =
-        float4{o.x * inv, o.y * inv, o.z * inv, o.w * inv};
-  }
+  const int L = max(0, min(Lraw, a.max_len));
+  if ((L + a.chunk - 1) / a.chunk <= 1) return;  // written directly by the attention kernel
+  merge_chunks<false>(a, s, hkv, Lraw);
 }
 
 static int occupancy_of(const hack_kv_layout& lay, int G) {
@@ -884,7 +940,8 @@ DecodePlan plan_decode(const hack_kv_layout& lay, int batch, int num_q_heads, in
   p.chunk = (int)(wg_spans * span);
   p.splits = max_len > 0 ? (int)(((int64_t)max_len + p.chunk - 1) / p.chunk) : 1;
   p.partial_floats = pairs * p.splits * G * (4 + lay.head_dim);
-  p.workspace_bytes = ((p.partial_floats * 4 + 255) / 256) * 256;
+  p.counter_offset = ((p.partial_floats * 4 + 255) / 256) * 256;
+  p.workspace_bytes = p.counter_offset + ((pairs * 4 + 255) / 256) * 256;
   return p;
 }
 
@@ -892,7 +949,7 @@ template <int BITS, int PI, int GT, int MODE>
 static hipError_t decode_impl(const DecodeArgs& a, int batch, hipStream_t stream) {
   dim3 grid((unsigned)a.splits, (unsigned)a.c.kv_heads, (unsigned)batch);
   hipLaunchKernelGGL((decode_kernel<BITS, PI, GT, MODE>), grid, dim3(256), 0, stream, a);
-  if (MODE == MODE_ATTEND && a.splits > 1)
+  if (MODE == MODE_ATTEND && a.splits > 1 && !HACK_DECODE_FUSED_MERGE)
     hipLaunchKernelGGL(decode_merge_kernel, dim3((unsigned)a.c.kv_heads, (unsigned)batch), dim3(256), 0, stream, a);
   return hipGetLastError();
 }

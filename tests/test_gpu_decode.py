@@ -147,3 +147,27 @@ def test_full_size_llama8b_decode_sampled():
     err = float(np.abs(got_rows - ref_rows).max() / np.abs(ref_rows).max())
     print(f"sampled rows max|d|/|O|inf = {err:.3e}")
     assert err <= TOL
+
+
+def test_split_merge_sees_each_calls_records():
+    """Back-to-back decode calls on one workspace with alternating queries: the chunk
+    records the merging workgroup reads must be the current call's (a stale record
+    of the previous call would give the other query's output)."""
+    gu = _gpu()
+    from paper_2502_03589_amd import hack as hk
+    from paper_2502_03589_amd import synth
+    gu.announce("split-K merge over repeated calls")
+    case = gu.Case(808, 4, 2, [2000, 1999, 1500, 2048], 2, 32, group=4).quantize()
+    qa = case.q
+    qb = synth.normal_f16(809, "q", qa.shape)
+    seqs = case.oracle_seqs()
+    refs = [O.attend_decode(q, seqs, case.H, 8, 0) for q in (qa, qb)]
+    qd = [torch.from_numpy(q).to(gu.DEV) for q in (qa, qb)]
+    ws = hk.decode_workspace(case.layout, case.batch, case.Hq, case.max_len)
+    outs = [torch.empty((case.batch, case.Hq, case.d), dtype=torch.float32, device=gu.DEV) for _ in range(40)]
+    for it, out in enumerate(outs):  # queued back to back, no host synchronization in between
+        hk.hack_attend_decode(case.layout, case.cache, qd[it % 2], case.lens_dev, case.max_len, out=out, workspace=ws)
+    torch.cuda.synchronize()
+    for it, out in enumerate(outs):
+        err = gu.rel_err(out.cpu().numpy(), refs[it % 2])
+        assert err <= TOL, f"call {it}: {err:.3e}"
