@@ -170,6 +170,23 @@ hack_status hack_attend_decode(const hack_kv_layout* layout, const hack_kv_cache
                                int32_t batch, int32_t max_len, int32_t tail_mode, float* out_dev,
                                void* workspace_dev, int64_t workspace_bytes, hipStream_t stream);
 
+/* One decode step (Sec. 5.3 with L_Q = 1, and the decode-side quantize-on-write of
+ * §6, fused in one launch): for every sequence s and kv head, the new token
+ * (k_new_dev / v_new_dev: fp16 [batch][H_kv][head_dim]) is written as token
+ * seq_lens_in[s] exactly as hack_append writes it (tail_mode as there), then the
+ * query q_dev attends over the seq_lens_in[s] + 1 cached tokens as in
+ * hack_attend_decode, and seq_lens_out[s] = seq_lens_in[s] + 1.  The two length
+ * arrays must be distinct (callers swap them between steps).  max_len bounds
+ * seq_lens_in; max_len + 1 must not exceed the capacity (HACK_ERR_CAPACITY).  The
+ * workspace is the one hack_decode_workspace_bytes(layout, batch, H_q, max_len + 1)
+ * sizes, zero-filled before first use as for hack_attend_decode. */
+hack_status hack_decode_step(const hack_kv_layout* layout, const hack_kv_cache* cache,
+                             const void* k_new_dev, const void* v_new_dev, const void* q_dev,
+                             int32_t num_q_heads, const int32_t* seq_lens_in_dev,
+                             int32_t* seq_lens_out_dev, int32_t batch, int32_t max_len,
+                             int32_t tail_mode, float* out_dev, void* workspace_dev,
+                             int64_t workspace_bytes, hipStream_t stream);
+
 /* Prefill attention of `len` query tokens per sequence over the quantized cache of
  * the same `len` tokens (Sec. 5.3 with L_Q = L_KV; Eq. 2-4), as written by
  * hack_quantize with all seq_lens = len.  q_dev: fp16 [batch][H_q][len][head_dim];

@@ -194,6 +194,40 @@ hack_status hack_attend_decode(const hack_kv_layout* layout, const hack_kv_cache
   return from_hip(hack::launch_decode(*layout, a, batch, hack::MODE_ATTEND, stream));
 }
 
+hack_status hack_decode_step(const hack_kv_layout* layout, const hack_kv_cache* cache, const void* k_new_dev,
+                             const void* v_new_dev, const void* q_dev, int32_t num_q_heads,
+                             const int32_t* seq_lens_in_dev, int32_t* seq_lens_out_dev, int32_t batch,
+                             int32_t max_len, int32_t tail_mode, float* out_dev, void* workspace_dev,
+                             int64_t workspace_bytes, hipStream_t stream) {
+  hack::DecodeArgs a;
+  int64_t cap = 0;
+  if (max_len < 0 || max_len == INT32_MAX) return HACK_ERR_INVALID_ARGUMENT;
+  // validated as a decode over max_len + 1 tokens
+  hack_status st = decode_common(layout, cache, q_dev, num_q_heads, seq_lens_in_dev, batch, max_len + 1, a, &cap);
+  if (st != HACK_OK) return st;
+  if (!k_new_dev || !v_new_dev || !seq_lens_out_dev || !out_dev || seq_lens_out_dev == seq_lens_in_dev ||
+      !(tail_mode == HACK_TAIL_FP16 || tail_mode == HACK_TAIL_REQUANT))
+    return HACK_ERR_INVALID_ARGUMENT;
+  const hack::DecodePlan plan = hack::plan_decode(*layout, batch, num_q_heads, max_len + 1);
+  if (!workspace_dev || workspace_bytes < plan.workspace_bytes) return HACK_ERR_WORKSPACE;
+  if (batch == 0) return HACK_OK;
+  a.out = out_dev;
+  a.partials = static_cast<float*>(workspace_dev);
+  a.counters = reinterpret_cast<int32_t*>(static_cast<uint8_t*>(workspace_dev) + plan.counter_offset);
+  a.chunk = plan.chunk;
+  a.splits = plan.splits;
+  a.tail_requant = tail_mode == HACK_TAIL_REQUANT;
+  a.k_new = static_cast<const __half*>(k_new_dev);
+  a.v_new = static_cast<const __half*>(v_new_dev);
+  a.lens_out = seq_lens_out_dev;
+  a.capacity = (int)cap;
+  a.stochastic = layout->rounding == HACK_ROUND_STOCHASTIC;
+  a.key_k = layout->seed ^ (1ull << 56);
+  a.key_v = layout->seed ^ (2ull << 56);
+  (void)hipGetLastError();
+  return from_hip(hack::launch_decode(*layout, a, batch, hack::MODE_ATTEND, stream));
+}
+
 hack_status hack_attend_prefill(const hack_kv_layout* layout, const hack_kv_cache* cache, const void* q_dev,
                                 int32_t num_q_heads, int32_t batch, int32_t len, int32_t causal, float* out_dev,
                                 hipStream_t stream) {

@@ -136,6 +136,77 @@ __device__ __forceinline__ uint64_t element_index(int s, int kv_heads, int h, in
   return ((((uint64_t)(s * kv_heads + h)) << 32) + (uint64_t)t) * (uint64_t)d + (uint64_t)ch;
 }
 
+template <int PI>
+__device__ __forceinline__ void load_f16_run(const __half* __restrict__ src, float (&x)[PI]) {
+  // PI contiguous fp16 values, 16 bytes at a time (PI is a multiple of 16).
+  const uint4* p = reinterpret_cast<const uint4*>(src);
+#pragma unroll
+  for (int i = 0; i < PI / 8; ++i) {
+    uint4 w = p[i];
+    const __half2* h = reinterpret_cast<const __half2*>(&w);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      float2 f = __half22float2(h[j]);
+      x[8 * i + 2 * j] = f.x;
+      x[8 * i + 2 * j + 1] = f.y;
+    }
+  }
+}
+
+template <int BITS, int PI>
+__device__ __forceinline__ void store_codes(uint8_t* dst, const uint32_t (&w)[(PI * BITS + 31) / 32]) {
+  uint32_t* d = reinterpret_cast<uint32_t*>(dst);
+#pragma unroll
+  for (int i = 0; i < (PI * BITS + 31) / 32; ++i) d[i] = w[i];
+}
+
+// Quantize-on-write of one token of one (sequence, kv head) (Sec. 5.3): the new
+// token is token L of the sequence.  Its K row is quantized per partition; its V
+// values go to row T = L mod PI of the fp16 open block, and the block is quantized
+// (n = T + 1 values per channel) when it fills or when `requant` is set.  Threads
+// tid < d/PI take one K partition each, threads tid, tid + nthreads, ... one V
+// channel each.  The caller guarantees 0 <= L < capacity.
+template <int BITS, int PI>
+__device__ __forceinline__ void append_head(const CacheView& c, const __half* __restrict__ k_new,
+                                            const __half* __restrict__ v_new, int s, int h, int L,
+                                            bool requant, bool stochastic, uint64_t key_k, uint64_t key_v,
+                                            int tid, int nthreads) {
+  const int H = c.kv_heads, d = c.head_dim, P = d / PI;
+  if (tid < P) {
+    float xk[PI];
+    load_f16_run<PI>(k_new + tid * PI, xk);
+    uint32_t words[(PI * BITS + 31) / 32];
+    uint16_t mb, sb;
+    const uint32_t sum = quantize_values<BITS, PI>(xk, PI, stochastic, key_k, element_index(s, H, h, L, d, tid * PI),
+                                                   1ull, words, mb, sb);
+    const int64_t row = k_row(c, s, h, L);
+    store_codes<BITS, PI>(c.k_codes + row * (d * BITS / 8) + tid * (PI * BITS / 8), words);
+    reinterpret_cast<uint32_t*>(c.k_meta)[row * P + tid] = (uint32_t)mb | ((uint32_t)sb << 16);
+    store_sum(c.k_sums, row * P + tid, c.sum_bytes, sum);
+  }
+  const int F = L / PI, T = L - F * PI;  // the new token is element T of block F
+  const bool quantize_v = T + 1 == PI || requant;
+  for (int ch = tid; ch < d; ch += nthreads) {
+    const __half vn = v_new[ch];
+    __half* tail = c.v_tail + (((int64_t)s * H + h) * PI) * d + ch;
+    tail[(int64_t)T * d] = vn;
+    if (quantize_v) {
+      float x[PI];
+#pragma unroll
+      for (int e = 0; e < PI; ++e)
+        x[e] = e < T ? __half2float(tail[(int64_t)e * d]) : (e == T ? __half2float(vn) : 0.0f);
+      uint32_t words[(PI * BITS + 31) / 32];
+      uint16_t mb, sb;
+      const uint32_t sum = quantize_values<BITS, PI>(x, T + 1, stochastic, key_v,
+                                                     element_index(s, H, h, F * PI, d, ch), (uint64_t)d, words, mb, sb);
+      const int64_t vbh = v_block<PI>(c, s, h, F * PI);
+      store_codes<BITS, PI>(c.v_codes + (vbh * d + ch) * (PI * BITS / 8), words);
+      reinterpret_cast<uint32_t*>(c.v_meta)[vbh * d + ch] = (uint32_t)mb | ((uint32_t)sb << 16);
+      store_sum(c.v_sums, vbh * d + ch, c.sum_bytes, sum);
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Cross-lane reductions inside a row of 16 lanes (DPP row rotates).
 // ---------------------------------------------------------------------------

@@ -46,6 +46,15 @@ struct DecodeArgs {
   int splits;
   int tail_requant;
   int max_len;
+  // fused append (hack_decode_step): when k_new is set, token lens[s] of every
+  // (sequence, kv head) is appended first, the attention covers lens[s] + 1 tokens
+  // and lens_out[s] = lens[s] + 1
+  const __half* k_new;    // [B][H_kv][128]
+  const __half* v_new;    // [B][H_kv][128]
+  int32_t* lens_out;      // [B]
+  int capacity;
+  int stochastic;
+  uint64_t key_k, key_v;
   // test exports
   uint8_t* dbg_qcodes;    // [B][H_q][128]
   float* dbg_qmeta;       // [B][H_q][P][2]

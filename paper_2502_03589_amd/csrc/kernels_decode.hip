@@ -336,8 +336,24 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
   const int G = a.group, Hq = a.num_q_heads, H = c.kv_heads;
   // lengths outside [0, max_len] break the caller contract; clamp so that every
   // access stays inside the cache and the workspace
-  const int L = max(0, min(a.lens[s], a.max_len));
+  const int Lin = a.lens[s];
+  int Lq = max(0, min(Lin, a.max_len));
   const int t0 = split * a.chunk;
+  if (MODE == MODE_ATTEND && a.k_new != nullptr) {
+    // decode step: append token Lin first (the workgroup whose chunk holds it), then
+    // attend over Lin + 1 tokens.  Other chunks never read the appended slots, and
+    // the new length goes to a separate array so no workgroup sees it half-way.
+    const bool ok = Lin >= 0 && Lin < a.capacity && Lin + 1 <= a.max_len;
+    Lq = ok ? Lin + 1 : Lq;
+    if (split == 0 && hkv == 0 && tid == 0) a.lens_out[s] = Lq;
+    if (ok && Lin / a.chunk == split) {
+      append_head<BITS, PI>(c, a.k_new + ((int64_t)s * H + hkv) * D, a.v_new + ((int64_t)s * H + hkv) * D, s, hkv,
+                            Lin, a.tail_requant != 0, a.stochastic != 0, a.key_k, a.key_v, tid, 256);
+      __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): the appended bytes are in L2
+      __syncthreads();
+    }
+  }
+  const int L = Lq;
   if (t0 >= L) {
     if (MODE == MODE_ATTEND && split == 0) {  // empty sequence: zeros
       for (int i = tid; i < G * D; i += 256) a.out[((int64_t)s * Hq + hkv * G) * D + i] = 0.0f;
@@ -904,7 +920,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
     }
     __syncthreads();
     if (last_chunk) {
-      merge_chunks<HACK_DECODE_FUSED_MERGE == 2>(a, s, hkv, a.lens[s]);
+      merge_chunks<HACK_DECODE_FUSED_MERGE == 2>(a, s, hkv, L);
       if (tid == 0) __hip_atomic_store(&a.counters[pair], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
@@ -914,7 +930,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
 // Split-K merge as a second launch: one workgroup per (sequence, kv head).
 __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeArgs a) {
   const int s = blockIdx.y, hkv = blockIdx.x;
-  const int Lraw = a.lens[s];
+  const int Lraw = a.k_new != nullptr ? a.lens[s] + 1 : a.lens[s];  // a decode step attends lens + 1
   const int L = max(0, min(Lraw, a.max_len));
   if ((L + a.chunk - 1) / a.chunk <= 1) return;  // written directly by the attention kernel
   merge_chunks<false>(a, s, hkv, Lraw);

@@ -8,30 +8,6 @@
 
 namespace hack {
 
-template <int PI>
-__device__ __forceinline__ void load_f16_run(const __half* __restrict__ src, float (&x)[PI]) {
-  // PI contiguous fp16 values, 16 bytes at a time (PI is a multiple of 16).
-  const uint4* p = reinterpret_cast<const uint4*>(src);
-#pragma unroll
-  for (int i = 0; i < PI / 8; ++i) {
-    uint4 w = p[i];
-    const __half2* h = reinterpret_cast<const __half2*>(&w);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      float2 f = __half22float2(h[j]);
-      x[8 * i + 2 * j] = f.x;
-      x[8 * i + 2 * j + 1] = f.y;
-    }
-  }
-}
-
-template <int BITS, int PI>
-__device__ __forceinline__ void store_codes(uint8_t* dst, const uint32_t (&w)[(PI * BITS + 31) / 32]) {
-  uint32_t* d = reinterpret_cast<uint32_t*>(dst);
-#pragma unroll
-  for (int i = 0; i < (PI * BITS + 31) / 32; ++i) d[i] = w[i];
-}
-
 template <int BITS, int PI>
 __global__ __launch_bounds__(256) void quantize_k_kernel(CacheView c, const __half* __restrict__ k,
                                                          const int32_t* __restrict__ lens, int batch,

@@ -59,6 +59,7 @@ _SIGS = {
     "hack_append": (_I32, [_LAY, _CAC, _P, _P, _P, _I32, _I32, _I32, _P]),
     "hack_decode_workspace_bytes": (_I64, [_LAY, _I32, _I32, _I32]),
     "hack_attend_decode": (_I32, [_LAY, _CAC, _P, _I32, _P, _I32, _I32, _I32, _P, _P, _I64, _P]),
+    "hack_decode_step": (_I32, [_LAY, _CAC, _P, _P, _P, _I32, _P, _P, _I32, _I32, _I32, _P, _P, _I64, _P]),
     "hack_attend_prefill": (_I32, [_LAY, _CAC, _P, _I32, _I32, _I32, _I32, _P, _P]),
     "hack_status_string": (ctypes.c_char_p, [_I32]),
     "hack_debug_qk_products": (_I32, [_LAY, _CAC, _P, _I32, _P, _I32, _I32, _P, _P, _P, _P]),
@@ -222,6 +223,26 @@ def hack_attend_decode(layout, cache: KVCache, q: torch.Tensor, seq_lens: torch.
     return out
 
 
+def hack_decode_step(layout, cache: KVCache, k_new: torch.Tensor, v_new: torch.Tensor, q: torch.Tensor,
+                     lens_in: torch.Tensor, lens_out: torch.Tensor, max_len: int, tail_mode: int = TAIL_FP16,
+                     out: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                     stream=None) -> torch.Tensor:
+    """Append one token per (sequence, kv head) and decode-attend over the longer
+    cache in one launch; lens_out = lens_in + 1.  `max_len` bounds lens_in."""
+    batch, hq, d = q.shape
+    if out is None:
+        out = torch.empty((batch, hq, d), dtype=torch.float32, device=q.device)
+    if workspace is None:
+        workspace = decode_workspace(layout, batch, hq, max_len + 1, q.device)
+    _check(lib().hack_decode_step(ctypes.byref(layout), ctypes.byref(cache.struct), _dev(k_new, torch.float16, "k_new"),
+                                  _dev(v_new, torch.float16, "v_new"), _dev(q, torch.float16, "q"), hq,
+                                  _dev(lens_in, torch.int32, "lens_in"), _dev(lens_out, torch.int32, "lens_out"),
+                                  batch, max_len, tail_mode, _dev(out, torch.float32, "out"),
+                                  _dev(workspace, torch.uint8, "workspace"), workspace.numel(), _stream(stream)),
+           "hack_decode_step")
+    return out
+
+
 def hack_attend_prefill(layout, cache: KVCache, q: torch.Tensor, causal: bool = True,
                         out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
     batch, hq, length, d = q.shape
@@ -285,3 +306,14 @@ def bind_attend_decode(layout, cache: KVCache, q, seq_lens, max_len: int, tail_m
                      _dev(q, torch.float16, "q"), hq, _dev(seq_lens, torch.int32, "seq_lens"), batch, max_len,
                      tail_mode, _dev(out, torch.float32, "out"), _dev(workspace, torch.uint8, "workspace"),
                      workspace.numel())
+
+
+def bind_decode_step(layout, cache: KVCache, k_new, v_new, q, lens_in, lens_out, max_len: int, tail_mode: int,
+                     out, workspace):
+    """Pre-marshalled hack_decode_step (see bind_append)."""
+    batch, hq, _ = q.shape
+    return BoundCall("hack_decode_step", "hack_decode_step", ctypes.byref(layout), ctypes.byref(cache.struct),
+                     _dev(k_new, torch.float16, "k_new"), _dev(v_new, torch.float16, "v_new"),
+                     _dev(q, torch.float16, "q"), hq, _dev(lens_in, torch.int32, "lens_in"),
+                     _dev(lens_out, torch.int32, "lens_out"), batch, max_len, tail_mode,
+                     _dev(out, torch.float32, "out"), _dev(workspace, torch.uint8, "workspace"), workspace.numel())

@@ -171,3 +171,49 @@ def test_split_merge_sees_each_calls_records():
     for it, out in enumerate(outs):
         err = gu.rel_err(out.cpu().numpy(), refs[it % 2])
         assert err <= TOL, f"call {it}: {err:.3e}"
+
+
+@pytest.mark.parametrize("bits,group,H,lens,tail_mode,paged", [
+    (2, 4, 2, [29, 31, 32, 100, 0], 0, 0),
+    (2, 4, 2, [29, 31, 32, 100, 0], 1, 0),
+    (2, 8, 1, [250, 255, 1000], 0, 256),
+    (4, 4, 2, [62, 63, 64], 1, 0),
+])
+def test_decode_step_equals_append_then_decode(bits, group, H, lens, tail_mode, paged):
+    """hack_decode_step (append fused into the attention launch) writes the same
+    cache bytes as hack_append and returns what hack_attend_decode returns after it,
+    over several steps that cross a block boundary; the end state matches the oracle."""
+    gu = _gpu()
+    from paper_2502_03589_amd import hack as hk
+    gu.announce(f"decode step bits={bits} G={group} H={H} lens={lens} tail={tail_mode} paged={paged}")
+    steps = 4
+    a = gu.Case(515 + bits, len(lens), H, lens, bits, 32, group=group, paged_page=paged, spare_tokens=steps).quantize()
+    b = gu.Case(515 + bits, len(lens), H, lens, bits, 32, group=group, paged_page=paged, spare_tokens=steps).quantize()
+    lens_in = b.lens_dev.clone()
+    lens_out = torch.zeros_like(lens_in)
+    for step in range(steps):
+        cur = a.lens_dev.cpu().numpy()
+        kn = torch.from_numpy(np.stack([a.k[s, :, cur[s]] for s in range(a.batch)])).to(gu.DEV)
+        vn = torch.from_numpy(np.stack([a.v[s, :, cur[s]] for s in range(a.batch)])).to(gu.DEV)
+        q = torch.from_numpy(synth_q(a, step)).to(gu.DEV)
+        ml = int(cur.max())
+        hk.hack_append(a.layout, a.cache, kn, vn, a.lens_dev, ml, tail_mode)
+        ref_out = hk.hack_attend_decode(a.layout, a.cache, q, a.lens_dev, ml + 1, tail_mode)
+        got = hk.hack_decode_step(b.layout, b.cache, kn, vn, q, lens_in, lens_out, ml, tail_mode)
+        torch.cuda.synchronize()
+        assert torch.equal(lens_out, a.lens_dev)
+        assert gu.rel_err(got.cpu().numpy(), ref_out.cpu().numpy().astype(np.float64)) <= 1e-5
+        lens_in, lens_out = lens_out, lens_in
+    ra, rb = a.sections(), b.sections()
+    for name in ra:
+        assert np.array_equal(ra[name], rb[name]), name
+    a.lens = a.lens_dev.cpu().numpy()
+    ref = O.attend_decode(synth_q(a, steps - 1), a.oracle_seqs(), H, 8, tail_mode)
+    err = gu.rel_err(got.cpu().numpy(), ref)
+    print(f"max|d|/|O|inf vs oracle after {steps} steps = {err:.3e}")
+    assert err <= TOL
+
+
+def synth_q(case, step):
+    from paper_2502_03589_amd import synth
+    return synth.normal_f16(case.seed + 1, "q", (case.batch, case.Hq, case.d), sub=step)
