@@ -112,6 +112,20 @@ constexpr float kMaxSlack = 8.0f;
 constexpr int kWaves = 4;
 constexpr int kComputeUnits = 256;  // MI355X
 
+// Waves per SIMD of the 2-bit, partition-32, one-row-tile kernel, and whether it
+// stages V through LDS with direct loads (needed to fit 128 VGPRs at four waves).
+// Measured: two waves per SIMD with V in registers is faster.  The compiler cannot
+// order direct-to-LDS loads with ordinary ones, so with V in LDS every wave waits
+// for all of its span's loads (vmcnt 0) before its first Q'K' product; with plain
+// loads the Q'K' tiles start as their own K data arrives, overlapping the rest.
+#ifndef HACK_DECODE_FAST_OCC
+#define HACK_DECODE_FAST_OCC 2
+#endif
+#ifndef HACK_DECODE_V_DMA
+#define HACK_DECODE_V_DMA 0
+#endif
+
+
 // Bytes of one cached code sum: 1 when b + ceil(log2 PI) <= 8, else 2 (Sec. 5.3).
 template <int BITS, int PI>
 constexpr int sum_width() {
@@ -126,7 +140,7 @@ constexpr int sum_width() {
 // tiles need more registers.
 template <int BITS, int PI, int GT>
 constexpr int decode_occupancy() {
-  return (BITS == 2 && PI == 32 && GT == 1) ? 4 : 2;
+  return (BITS == 2 && PI == 32 && GT == 1) ? HACK_DECODE_FAST_OCC : 2;
 }
 
 #ifndef HACK_DECODE_FUSED_MERGE
@@ -206,7 +220,7 @@ struct VStage {
 // whose register budget cannot also hold a span's V data).
 template <int BITS, int PI, int GT>
 constexpr bool decode_v_in_lds() {
-  return decode_occupancy<BITS, PI, GT>() == 4;
+  return decode_occupancy<BITS, PI, GT>() == 4 && HACK_DECODE_V_DMA;
 }
 
 // LDS of one wave.
