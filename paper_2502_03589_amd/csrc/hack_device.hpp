@@ -191,10 +191,14 @@ __device__ __forceinline__ void append_head(const CacheView& c, const __half* __
     __half* tail = c.v_tail + (((int64_t)s * H + h) * PI) * d + ch;
     tail[(int64_t)T * d] = vn;
     if (quantize_v) {
+      // every row of the open block is read (rows past T are ignored), so the loads
+      // are independent of T and issue together
+      __half raw[PI];
+#pragma unroll
+      for (int e = 0; e < PI; ++e) raw[e] = tail[(int64_t)e * d];
       float x[PI];
 #pragma unroll
-      for (int e = 0; e < PI; ++e)
-        x[e] = e < T ? __half2float(tail[(int64_t)e * d]) : (e == T ? __half2float(vn) : 0.0f);
+      for (int e = 0; e < PI; ++e) x[e] = e < T ? __half2float(raw[e]) : (e == T ? __half2float(vn) : 0.0f);
       uint32_t words[(PI * BITS + 31) / 32];
       uint16_t mb, sb;
       const uint32_t sum = quantize_values<BITS, PI>(x, T + 1, stochastic, key_v,

@@ -147,6 +147,10 @@ constexpr int decode_occupancy() {
 #define HACK_DECODE_FUSED_MERGE 2  // 1/2: the last chunk of a sequence merges (else a second launch)
 #endif
 
+#ifndef HACK_DECODE_SPAN_ROUND
+#define HACK_DECODE_SPAN_ROUND 1
+#endif
+
 #ifndef HACK_DECODE_WGS_PER_CU
 #define HACK_DECODE_WGS_PER_CU 0  // 0: the kernel's occupancy
 #endif
@@ -950,9 +954,12 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeArgs a) {
   merge_chunks<false>(a, s, hkv, Lraw);
 }
 
+// Workgroups per compute unit the grid is sized for.  The 2-bit, partition-32 kernel
+// with one row tile uses about 145 VGPRs, so three waves per SIMD are resident even
+// though it is compiled for two (measured best on the 4K-context decode workload).
 static int occupancy_of(const hack_kv_layout& lay, int G) {
   const int gt = G <= 4 ? 1 : 2;
-  if (lay.kv_bits == 2 && lay.partition == 32 && gt == 1) return decode_occupancy<2, 32, 1>();
+  if (lay.kv_bits == 2 && lay.partition == 32 && gt == 1) return decode_occupancy<2, 32, 1>() + 1;
   return 2;
 }
 
@@ -967,6 +974,8 @@ DecodePlan plan_decode(const hack_kv_layout& lay, int batch, int num_q_heads, in
   const int64_t spans_seq = ((int64_t)max_len + span - 1) / span;
   int64_t wg_spans = pairs > 0 ? (spans_seq * pairs + target - 1) / target : 1;
   if (wg_spans < 1) wg_spans = 1;
+  if (HACK_DECODE_SPAN_ROUND > 1 && wg_spans > kWaves)  // whole spans for every wave of a workgroup
+    wg_spans = (wg_spans + HACK_DECODE_SPAN_ROUND - 1) / HACK_DECODE_SPAN_ROUND * HACK_DECODE_SPAN_ROUND;
   p.chunk = (int)(wg_spans * span);
   p.splits = max_len > 0 ? (int)(((int64_t)max_len + p.chunk - 1) / p.chunk) : 1;
   p.partial_floats = pairs * p.splits * G * (4 + lay.head_dim);

@@ -122,10 +122,13 @@ __global__ __launch_bounds__(256) void append_kernel(CacheView c, const __half* 
     tail[(int64_t)T * d] = vn[i];
     if (quantize_v) {
       const int n = T + 1;
+      // every row of the open block is read (rows past T are ignored): independent loads
+      __half raw[PI];
+#pragma unroll
+      for (int e = 0; e < PI; ++e) raw[e] = tail[(int64_t)e * d];
       float x[PI];
 #pragma unroll
-      for (int e = 0; e < PI; ++e)
-        x[e] = e < T ? __half2float(tail[(int64_t)e * d]) : (e == T ? __half2float(vn[i]) : 0.0f);
+      for (int e = 0; e < PI; ++e) x[e] = e < T ? __half2float(raw[e]) : (e == T ? __half2float(vn[i]) : 0.0f);
       uint32_t words[(PI * BITS + 31) / 32];
       uint16_t mb, sb;
       const uint32_t sum = quantize_values<BITS, PI>(

@@ -13,7 +13,8 @@ from typing import Optional
 
 import torch
 
-_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhack.so")
+# HACK_LIBRARY may point at another build of the library (e.g. a tuning variant)
+_LIB_PATH = os.environ.get("HACK_LIBRARY") or os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhack.so")
 _lib = None
 
 HACK_OK = 0
