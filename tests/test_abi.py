@@ -130,7 +130,21 @@ def test_argument_errors_before_launch(lib):
     lay128 = hk.hack_kv_layout_make(128, 2, 2, 128, 128)
     assert lib.hack_attend_prefill(ctypes.byref(lay128), C, p, 8, 2, 100, 1, p, None) == 2
     assert lib.hack_attend_prefill(L, C, p, 8, 2, 129, 1, p, None) == 3
+    # decode step: capacity counts the appended token, length arrays must differ,
+    # workspace is sized for max_len + 1, paged caches need pages of 4 * partition
+    p2 = ctypes.c_void_p(0x6000)
+    wss = hk.hack_decode_workspace_bytes(lay, 2, 8, 101)
+    assert lib.hack_decode_step(L, C, p, p, p, 8, p, p2, 2, 128, 0, p, p, 10 ** 9, None) == 3
+    assert lib.hack_decode_step(L, C, p, p, p, 8, p, p, 2, 100, 0, p, p, 10 ** 9, None) == 1
+    assert lib.hack_decode_step(L, C, None, p, p, 8, p, p2, 2, 100, 0, p, p, 10 ** 9, None) == 1
+    assert lib.hack_decode_step(L, C, p, p, p, 8, p, p2, 2, 100, 7, p, p, 10 ** 9, None) == 1
+    assert lib.hack_decode_step(L, C, p, p, p, 8, p, p2, 2, 100, 0, p, p, wss - 1, None) == 4
+    lay_pg = hk.hack_kv_layout_make(128, 2, 2, 32, 64)
+    paged64 = _Fake(pages=4, table=True, mbps=3)
+    assert lib.hack_attend_decode(ctypes.byref(lay_pg), ctypes.byref(paged64.struct), p, 8, p, 2, 100, 0, p, p,
+                                  10 ** 9, None) == 2
     # zero-sized work is a no-op that succeeds without launching
+    assert lib.hack_decode_step(L, C, p, p, p, 8, p, p2, 0, 10, 0, p, p, 10 ** 9, None) == 0
     assert lib.hack_quantize(L, C, p, p, p, 0, 10, None) == 0
     assert lib.hack_attend_prefill(L, C, p, 8, 2, 0, 1, p, None) == 0
 
