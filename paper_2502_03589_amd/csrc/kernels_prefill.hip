@@ -247,8 +247,12 @@ __device__ __forceinline__ void stage_store(const StageRegs<BITS, PI>& r, Stage<
 
 }  // namespace
 
+// Two workgroups per compute unit (four waves per SIMD, 128 VGPRs each; the two
+// workgroups' LDS, about 78 KB each for partition 64, fits the 160 KB of a CU), so
+// that one workgroup's block barrier and staging overlap the other's arithmetic
+// (measured 1.61 -> 1.36-1.44 ms on the 8K causal prefill).
 template <int BITS, int PI>
-__global__ __launch_bounds__(512, 1) void prefill_kernel(PrefillArgs a) {
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4))) void prefill_kernel(PrefillArgs a) {
   using C = PrefillCfg<PI>;
   using OP = Op<PI>;
   typedef typename OP::T opT;
