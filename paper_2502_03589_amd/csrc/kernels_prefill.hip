@@ -191,6 +191,28 @@ __device__ __forceinline__ void stage_load(const PrefillArgs& a, StageRegs<BITS,
   }
 }
 
+// One dword of packed codes (element e in bits [BITS*e, BITS*e + BITS)) expanded to
+// one byte per element in element order: masks pick every other (4-bit) or every
+// fourth (2-bit) element, byte permutes interleave them back.
+template <int BITS>
+__device__ __forceinline__ void expand_word(uint32_t x, uint32_t* out) {
+  if constexpr (BITS == 4) {
+    const uint32_t lo = x & 0x0F0F0F0Fu, hi = (x >> 4) & 0x0F0F0F0Fu;  // elements 0,2,4,6 | 1,3,5,7
+    out[0] = __builtin_amdgcn_perm(hi, lo, 0x05010400u);
+    out[1] = __builtin_amdgcn_perm(hi, lo, 0x07030602u);
+  } else {
+    uint32_t d[4];  // d[k] byte j = element 4j + k
+#pragma unroll
+    for (int k = 0; k < 4; ++k) d[k] = (x >> (2 * k)) & 0x03030303u;
+    const uint32_t a0 = __builtin_amdgcn_perm(d[1], d[0], 0x05010400u), a1 = __builtin_amdgcn_perm(d[1], d[0], 0x07030602u);
+    const uint32_t b0 = __builtin_amdgcn_perm(d[3], d[2], 0x05010400u), b1 = __builtin_amdgcn_perm(d[3], d[2], 0x07030602u);
+    out[0] = __builtin_amdgcn_perm(b0, a0, 0x05040100u);
+    out[1] = __builtin_amdgcn_perm(b0, a0, 0x07060302u);
+    out[2] = __builtin_amdgcn_perm(b1, a1, 0x05040100u);
+    out[3] = __builtin_amdgcn_perm(b1, a1, 0x07060302u);
+  }
+}
+
 template <int BITS, int PI>
 __device__ __forceinline__ void stage_store(const StageRegs<BITS, PI>& r, Stage<PI>& st, bool with_v) {
   using C = PrefillCfg<PI>;
@@ -201,16 +223,11 @@ __device__ __forceinline__ void stage_store(const StageRegs<BITS, PI>& r, Stage<
     // K codes unpacked to int8 in channel order
     const int tt = tid / TPR, cb = (tid % TPR) * CPT;
     uint32_t* dst = reinterpret_cast<uint32_t*>(&st.k[tt][cb]);
+    uint32_t bytes[CPT / 4];
 #pragma unroll
-    for (int e4 = 0; e4 < CPT / 4; ++e4) {
-      uint32_t v = 0;
+    for (int i = 0; i < StageRegs<BITS, PI>::KW; ++i) expand_word<BITS>(r.w[i], bytes + i * (32 / BITS) / 4);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int e = 4 * e4 + i;
-        v |= ((r.w[(e * BITS) / 32] >> ((e * BITS) % 32)) & ((1u << BITS) - 1)) << (8 * i);
-      }
-      dst[e4] = v;
-    }
+    for (int e4 = 0; e4 < CPT / 4; ++e4) dst[e4] = bytes[e4];
     if (tid < PI * P) {
       const int tt2 = tid / P, p = tid % P;
       const float mk = __half2float(__ushort_as_half((uint16_t)(r.meta & 0xFFFFu)));
@@ -223,14 +240,12 @@ __device__ __forceinline__ void stage_store(const StageRegs<BITS, PI>& r, Stage<
     // V codes: token tau = 16*tl + 4*g + i goes to operand position g*KSL + 4*tl + i
     const int vt = tid - 256;
     const int ch = vt >> 1, half = vt & 1;
+    uint32_t bytes[PI / 8];
+#pragma unroll
+    for (int i = 0; i < StageRegs<BITS, PI>::KW; ++i) expand_word<BITS>(r.w[i], bytes + i * (32 / BITS) / 4);
 #pragma unroll
     for (int q4 = 0; q4 < PI / 8; ++q4) {
-      uint32_t v = 0;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int e = 4 * q4 + i;
-        v |= ((r.w[(e * BITS) / 32] >> ((e * BITS) % 32)) & ((1u << BITS) - 1)) << (8 * i);
-      }
+      const uint32_t v = bytes[q4];
       const int tau0 = half * (PI / 2) + 4 * q4;
       const int tl = tau0 >> 4, g = (tau0 >> 2) & 3;
       *reinterpret_cast<uint32_t*>(&st.v[ch][g * KSL + 4 * tl]) = v;
