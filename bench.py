@@ -2,11 +2,12 @@
 
 Default workload: Llama-3-8B-shaped decode (batch 16, 32 q heads / 8 kv heads,
 head_dim 128, context 4096, 2-bit K/V with partition 32, 4 K channels x10).
-One step = quantize-on-write of one new token per sequence (hack_append) plus
-decode attention over the whole compressed cache (hack_attend_decode).  Ten
-replicas of the cache rotate so that the 256 MB Infinity Cache cannot hold the
+One step = one hack_decode_step launch: quantize-on-write of one new token per
+(sequence, kv head) fused with decode attention over the whole compressed cache.
+Ten replicas of the cache rotate so that the 256 MB Infinity Cache cannot hold the
 working set.  Also measured: causal prefill (batch 1, 32/8 heads, 8192 tokens,
-4-bit K/V, partition 64) when the kernel is available.
+4-bit K/V, partition 64).  --workload selects another decode workload instead
+(ragged paged 70B share, 128K append loop, or the bit-width/partition sweep).
 
 Prints ONE JSON line.  `value` is compressed bytes moved per step / step time.
 """
@@ -76,7 +77,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prefill", action="store_true")
     ap.add_argument("--prefill-iters", type=int, default=10)
-    ap.add_argument("--workload", choices=["decode_70b_ragged", "decode_long_l131072"], default=None,
+    ap.add_argument("--workload", choices=["decode_70b_ragged", "decode_long_l131072", "sweep_bits_partition"],
+                    default=None,
                     help="time another decode workload instead (one JSON line per configuration; "
                          "not the headline line)")
     ap.add_argument("--only", choices=["decode", "prefill", "copy"], default=None,
@@ -299,7 +301,7 @@ def bench_workload(name: str, steps: int, warmup: int):
     from paper_2502_03589_amd import hack as hk
     from paper_2502_03589_amd import synth
     dev = torch.device("cuda:0")
-    wl = synth.WORKLOADS[name]
+    wl = synth.WORKLOADS[name if name != "sweep_bits_partition" else "decode_llama8b_l4096"]
     B, Hq, H, d, pi = wl.batch, wl.q_heads, wl.kv_heads, wl.head_dim, wl.partition
 
     def timed(fn, n):
@@ -311,6 +313,41 @@ def bench_workload(name: str, steps: int, warmup: int):
         torch.cuda.synchronize()
         return float(np.mean([a.elapsed_time(b) for a, b in ev]))
 
+    if name == "sweep_bits_partition":
+        # decode_llama8b_l4096's shapes and inputs for each code width and partition the
+        # kernels support (attention only, over replicated caches)
+        base = synth.WORKLOADS["decode_llama8b_l4096"]
+        B, Hq, H, d, L = base.batch, base.q_heads, base.kv_heads, base.head_dim, base.context
+        k = torch.from_numpy(synth.normal_f16(base.seed, "k", (B, H, L, d))).to(dev)
+        v = torch.from_numpy(synth.normal_f16(base.seed, "v", (B, H, L, d))).to(dev)
+        q = torch.from_numpy(synth.normal_f16(base.seed, "q", (B, Hq, d))).to(dev)
+        ln = torch.full((B,), L, dtype=torch.int32, device=dev)
+        R = 10
+        for bits, part in ((2, 32), (2, 64), (4, 32), (4, 64)):
+            lay = hk.hack_kv_layout_make(d, H, bits, part, L)
+            caches = [hk.KVCache(lay, B, B, None, dev) for _ in range(R)]
+            for cache in caches:
+                hk.hack_quantize(lay, cache, k, v, ln, L)
+            ws = hk.decode_workspace(lay, B, Hq, L)
+            out = torch.empty((B, Hq, d), dtype=torch.float32, device=dev)
+            calls = [hk.bind_attend_decode(lay, cache, q, ln, L, hk.TAIL_FP16, out, ws) for cache in caches]
+            for i in range(warmup):
+                calls[i % R]()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for i in range(steps):
+                calls[i % R]()
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / steps
+            nbytes = B * H * decode_bytes_per_seq_head(L, d, bits, part, lay.sum_bytes) + B * Hq * d * 6
+            print(json.dumps({"workload": name, "kv_bits": bits, "partition": part, "metric": "decode GB/s",
+                              "value": round(nbytes / ms / 1e6, 2), "unit": "GB/s", "us_per_call": round(ms * 1e3, 2),
+                              "bytes_per_call": int(nbytes), "bytes_per_token_head": round(nbytes / (B * H * L), 2),
+                              "frac_of_8TBs": round(nbytes / ms / 1e6 / HBM_PEAK_GBS, 4)}), flush=True)
+            del caches, calls
+        return
     if name == "decode_70b_ragged":
         lens = synth.uniform_lengths(wl.seed, B, *wl.len_range)
         table, pages = synth.page_table(wl.seed, lens, wl.page_tokens)
