@@ -45,7 +45,10 @@ constexpr float kSlack = 8.0f;   // reference max raised only beyond this (log2 
 #define HACK_PREFILL_QK_RANK_MFMA 1  // Q'K' rank-1 terms as outer-product MFMAs (else VALU)
 #endif
 #ifndef HACK_PREFILL_PV_RANK_MFMA
-#define HACK_PREFILL_PV_RANK_MFMA 0  // P'V' rank-1 terms as outer-product MFMAs (else VALU)
+#define HACK_PREFILL_PV_RANK_MFMA 0  // P'V' rank-1 terms as one outer-product MFMA per block
+#endif
+#ifndef HACK_PREFILL_PV_RANK_PAIRED
+#define HACK_PREFILL_PV_RANK_PAIRED 1  // ... as one outer-product MFMA per two blocks (else VALU)
 #endif
 
 template <int PI>
@@ -89,13 +92,17 @@ struct Op<32> {
   }
 };
 
+// V metadata of one block, per channel: s_v, m_v, s_v*sum v' + PI*m_v.  Kept in a
+// ring of three (block kb in slot kb % 3) apart from the two K/V code stages, so
+// that a block's metadata outlives its codes by one block.
+typedef float VMeta[3][128];
+
 // LDS of one staged V block.
 template <int PI>
 struct Stage {
   int8_t k[PI][PrefillCfg<PI>::KROW];          // K codes, [token][channel]
   int8_t v[128][PrefillCfg<PI>::VROW];         // V codes, [channel][operand position]
   float km[PrefillCfg<PI>::P][3][PI];          // per token and partition: s_k, s_k*sum k', m_k
-  float vm[3][128];                            // per channel: s_v, m_v, s_v*sum v' + PI*m_v
 };
 
 __device__ __forceinline__ v4f mfma_f32(float a, float b, v4f c) {
@@ -214,7 +221,7 @@ __device__ __forceinline__ void expand_word(uint32_t x, uint32_t* out) {
 }
 
 template <int BITS, int PI>
-__device__ __forceinline__ void stage_store(const StageRegs<BITS, PI>& r, Stage<PI>& st, bool with_v) {
+__device__ __forceinline__ void stage_store(const StageRegs<BITS, PI>& r, Stage<PI>& st, VMeta& vm, bool with_v) {
   using C = PrefillCfg<PI>;
   constexpr int D = 128, P = C::P, KSL = C::KSL;
   constexpr int CPT = PI / 2, TPR = D / CPT;
@@ -253,9 +260,9 @@ __device__ __forceinline__ void stage_store(const StageRegs<BITS, PI>& r, Stage<
     if (vt < D) {
       const float mv = __half2float(__ushort_as_half((uint16_t)(r.meta & 0xFFFFu)));
       const float sv = __half2float(__ushort_as_half((uint16_t)(r.meta >> 16)));
-      st.vm[0][vt] = sv;
-      st.vm[1][vt] = mv;
-      st.vm[2][vt] = fmaf((float)PI, mv, sv * (float)r.sum);
+      vm[0][vt] = sv;
+      vm[1][vt] = mv;
+      vm[2][vt] = fmaf((float)PI, mv, sv * (float)r.sum);
     }
   }
 }
@@ -274,6 +281,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
   constexpr int D = 128, P = C::P, TL = C::TL, KSL = C::KSL;
 
   __shared__ __attribute__((aligned(16))) Stage<PI> stages[2];
+  __shared__ __attribute__((aligned(16))) VMeta vm_ring[3];
   __shared__ float ptail[8][16][PI];
 
   const CacheView& c = a.c;
@@ -362,16 +370,32 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
   v4f o[8];
 #pragma unroll
   for (int j = 0; j < 8; ++j) o[j] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+  // P'V' rank-1 terms of two V blocks go into one f32 MFMA per 16 channels (its four
+  // k slots: (s_p sum p~', m~_p) of each block against (m_v, s_v sum v' + n m_v)).
+  // The row-side pair of the first block waits here; that block's stage stays
+  // intact until the end of the next iteration.
+  float rk_pz = 0.0f, rk_pm = 0.0f;
+  int rk_blk = -1;
+  auto rank_pair = [&](const VMeta& vm1, float pz1, float pm1, bool have1) __attribute__((always_inline)) {
+    const VMeta& vm0 = vm_ring[rk_blk % 3];
+    const float b = grp == 0 ? rk_pz : (grp == 1 ? rk_pm : (grp == 2 ? pz1 : pm1));
+    const float* src = grp < 2 ? &vm0[1 + (grp & 1)][col] : &vm1[1 + (grp & 1)][col];
+    const bool live = grp < 2 || have1;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) o[j] = mfma_f32(live ? src[16 * j] : 0.0f, live ? b : 0.0f, o[j]);
+    rk_blk = -1;
+  };
 
   StageRegs<BITS, PI> sr;
   if (nblk > 0) {
     stage_load<BITS, PI>(a, sr, s, hkv, 0, 0 < F);
-    stage_store<BITS, PI>(sr, stages[0], 0 < F);
+    stage_store<BITS, PI>(sr, stages[0], vm_ring[0], 0 < F);
   }
   __syncthreads();
 
   for (int kb = 0; kb < nblk; ++kb) {
     Stage<PI>& st = stages[kb & 1];
+    const VMeta& vmc = vm_ring[kb % 3];
     const bool next = kb + 1 < nblk;
     if (next) stage_load<BITS, PI>(a, sr, s, hkv, kb + 1, kb + 1 < F);
     const bool is_tail = kb >= F;  // the fp16 open block
@@ -446,6 +470,8 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
       l_run *= alpha;
 #pragma unroll
       for (int j = 0; j < 8; ++j) o[j] *= alpha;
+      rk_pz *= alpha;
+      rk_pm *= alpha;
       m_ref = bmax;
     }
     float pt[TL][4];
@@ -491,13 +517,14 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
         const opT va = OP::lds(&st.v[cc][grp * KSL]);
         const v4i acc = OP::mfma(va, pop, v4i{0, 0, 0, 0});
         // (s_p sum p~') m_v + m~_p (s_v sum v' + n m_v), then s_p s_v D~
-#if HACK_PREFILL_PV_RANK_MFMA
-        const float avr = grp == 0 ? st.vm[1][cc] : (grp == 1 ? st.vm[2][cc] : 0.0f);
+#if HACK_PREFILL_PV_RANK_PAIRED
+#elif HACK_PREFILL_PV_RANK_MFMA
+        const float avr = grp == 0 ? vmc[1][cc] : (grp == 1 ? vmc[2][cc] : 0.0f);
         o[j] = mfma_f32(avr, bpr, o[j]);
 #else
         {
-          const float4 fm = *reinterpret_cast<const float4*>(&st.vm[1][16 * j + 4 * grp]);
-          const float4 fb = *reinterpret_cast<const float4*>(&st.vm[2][16 * j + 4 * grp]);
+          const float4 fm = *reinterpret_cast<const float4*>(&vmc[1][16 * j + 4 * grp]);
+          const float4 fb = *reinterpret_cast<const float4*>(&vmc[2][16 * j + 4 * grp]);
           const float vmn[4] = {fm.x, fm.y, fm.z, fm.w};
           const float vbar[4] = {fb.x, fb.y, fb.z, fb.w};
 #pragma unroll
@@ -505,18 +532,30 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
         }
 #endif
 #if HACK_PREFILL_SCALE_MFMA
-        const float avs = grp == 0 ? st.vm[0][cc] : 0.0f;
+        const float avs = grp == 0 ? vmc[0][cc] : 0.0f;
         const v4f spv = mfma_f32(avs, bps, v4f{0.0f, 0.0f, 0.0f, 0.0f});
 #pragma unroll
         for (int i = 0; i < 4; ++i) o[j][i] = fmaf(spv[i], (float)acc[i], o[j][i]);
 #else
-        const float4 fs = *reinterpret_cast<const float4*>(&st.vm[0][16 * j + 4 * grp]);
+        const float4 fs = *reinterpret_cast<const float4*>(&vmc[0][16 * j + 4 * grp]);
         const float vs[4] = {fs.x, fs.y, fs.z, fs.w};
 #pragma unroll
         for (int i = 0; i < 4; ++i) o[j][i] = fmaf(ps * vs[i], (float)acc[i], o[j][i]);
 #endif
       }
+#if HACK_PREFILL_PV_RANK_PAIRED
+      if (rk_blk < 0) {
+        rk_pz = pz;
+        rk_pm = pm;
+        rk_blk = kb;
+      } else {
+        rank_pair(vmc, pz, pm, true);
+      }
+#endif
     } else {
+#if HACK_PREFILL_PV_RANK_PAIRED
+      if (rk_blk >= 0) rank_pair(vmc, 0.0f, 0.0f, false);
+#endif
       // fp16 open block: O[row][ch] += sum_{t < T} p[row][t] v_t[ch] with unquantized p
 #pragma unroll
       for (int tl = 0; tl < TL; ++tl)
@@ -539,10 +578,13 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
         }
       }
     }
-    if (next) stage_store<BITS, PI>(sr, stages[(kb + 1) & 1], kb + 1 < F);
+    if (next) stage_store<BITS, PI>(sr, stages[(kb + 1) & 1], vm_ring[(kb + 1) % 3], kb + 1 < F);
     __syncthreads();  // stage kb+1 complete; stage kb free for kb+2
   }
 
+#if HACK_PREFILL_PV_RANK_PAIRED
+  if (rk_blk >= 0) rank_pair(vm_ring[0], 0.0f, 0.0f, false);
+#endif
   // ---- normalize and write O[row][16 j + 4 grp + i] ----
   const float lsum = xg_sum(l_run);
   if (head_ok && row < L) {
