@@ -163,8 +163,8 @@ int64_t hack_decode_workspace_bytes(const hack_kv_layout* layout, int32_t batch,
  * chunk records) and must not be shared by calls that may run concurrently.  One
  * kernel is launched; when a sequence is split into several chunks, the workgroup
  * that finishes its last chunk merges them.
- * Requires head_dim 128, partition 32 or 64, H_q/H_kv <= 8 and, for a paged cache,
- * page_tokens a multiple of 4 * partition (else HACK_ERR_UNSUPPORTED). */
+ * Requires head_dim 128, partition 32 or 64, H_q/H_kv <= 8, batch <= 65535 and, for
+ * a paged cache, page_tokens a multiple of 4 * partition (else HACK_ERR_UNSUPPORTED). */
 hack_status hack_attend_decode(const hack_kv_layout* layout, const hack_kv_cache* cache,
                                const void* q_dev, int32_t num_q_heads, const int32_t* seq_lens_dev,
                                int32_t batch, int32_t max_len, int32_t tail_mode, float* out_dev,
@@ -193,7 +193,7 @@ hack_status hack_decode_step(const hack_kv_layout* layout, const hack_kv_cache* 
  * out_dev: fp32 [batch][H_q][len][head_dim].  causal != 0 masks token j > i for
  * query i; the masked zeros of P inside a block are quantized with the block.  The
  * open V block is used in fp16.  Requires head_dim 128, partition 32 or 64,
- * H_q % H_kv == 0 and H_q/H_kv <= 8 (else HACK_ERR_UNSUPPORTED). */
+ * H_q % H_kv == 0, H_q/H_kv <= 8 and batch <= 65535 (else HACK_ERR_UNSUPPORTED). */
 hack_status hack_attend_prefill(const hack_kv_layout* layout, const hack_kv_cache* cache,
                                 const void* q_dev, int32_t num_q_heads, int32_t batch, int32_t len,
                                 int32_t causal, float* out_dev, hipStream_t stream);

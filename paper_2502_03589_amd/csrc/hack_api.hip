@@ -8,6 +8,8 @@ using hack::CacheView;
 
 namespace {
 
+constexpr int kMaxGridYZ = 65535;  // largest y or z extent of a launch grid
+
 bool layout_ok(const hack_kv_layout* l) {
   if (!l) return false;
   const int pi = l->partition;
@@ -155,6 +157,7 @@ static hack_status decode_common(const hack_kv_layout* layout, const hack_kv_cac
     return HACK_ERR_INVALID_ARGUMENT;
   const hack_status sh = attention_shape(layout, num_q_heads);
   if (sh != HACK_OK) return sh;
+  if (batch > kMaxGridYZ) return HACK_ERR_UNSUPPORTED;  // one grid row per sequence
   const int64_t cap = cache_capacity(layout, cache, batch);
   if (cap < 0) return HACK_ERR_INVALID_ARGUMENT;
   if (max_len > cap) return HACK_ERR_CAPACITY;
@@ -234,6 +237,7 @@ hack_status hack_attend_prefill(const hack_kv_layout* layout, const hack_kv_cach
   if (!layout_ok(layout) || !q_dev || !out_dev || batch < 0 || len < 0) return HACK_ERR_INVALID_ARGUMENT;
   const hack_status sh = attention_shape(layout, num_q_heads);
   if (sh != HACK_OK) return sh;
+  if (batch > kMaxGridYZ) return HACK_ERR_UNSUPPORTED;  // one grid plane per sequence
   const int64_t cap = cache_capacity(layout, cache, batch);
   if (cap < 0) return HACK_ERR_INVALID_ARGUMENT;
   if (len > cap) return HACK_ERR_CAPACITY;

@@ -26,6 +26,7 @@
 //         re-quantized codes with n = T (TAIL_REQUANT).
 // The four waves merge in LDS; when a sequence spans several chunks, each chunk's
 // partial (max, sum, O) goes to the workspace and a second, small kernel merges them.
+#include <algorithm>
 #include <type_traits>
 
 #include "hack_internal.hpp"
@@ -350,7 +351,10 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
   // wave index made explicitly wave-uniform so span bookkeeping stays in scalar registers
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int col = lane & 15, grp = lane >> 4;
-  const int s = blockIdx.z, hkv = blockIdx.y, split = blockIdx.x;
+  // chunk index slowest: every (sequence, head) pair's first chunks are dispatched
+  // before any pair's later ones, so a long sequence's chunks do not queue behind
+  // the short sequences of a ragged batch
+  const int s = blockIdx.y, hkv = blockIdx.x, split = blockIdx.z;
   const int G = a.group, Hq = a.num_q_heads, H = c.kv_heads;
   // lengths outside [0, max_len] break the caller contract; clamp so that every
   // access stays inside the cache and the workspace
@@ -954,6 +958,9 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeArgs a) {
   merge_chunks<false>(a, s, hkv, Lraw);
 }
 
+constexpr int64_t kMaxWgSpans = 64;
+constexpr int64_t kMaxGridZ = 65535;
+
 // Workgroups per compute unit the grid is sized for.  The 2-bit, partition-32 kernel
 // with one row tile uses about 145 VGPRs, so three waves per SIMD are resident even
 // though it is compiled for two (measured best on the 4K-context decode workload).
@@ -974,6 +981,12 @@ DecodePlan plan_decode(const hack_kv_layout& lay, int batch, int num_q_heads, in
   const int64_t spans_seq = ((int64_t)max_len + span - 1) / span;
   int64_t wg_spans = pairs > 0 ? (spans_seq * pairs + target - 1) / target : 1;
   if (wg_spans < 1) wg_spans = 1;
+  // A chunk of at most kMaxWgSpans spans bounds the time one workgroup holds a slot:
+  // in a ragged batch the longest sequence then spreads over more workgroups than an
+  // even share of the mean length would give it.  The grid's z extent (the splits)
+  // stays within its 65535 limit.
+  if (wg_spans > kMaxWgSpans) wg_spans = kMaxWgSpans;
+  wg_spans = std::max<int64_t>(wg_spans, (spans_seq + kMaxGridZ - 1) / kMaxGridZ);
   if (HACK_DECODE_SPAN_ROUND > 1 && wg_spans > kWaves)  // whole spans for every wave of a workgroup
     wg_spans = (wg_spans + HACK_DECODE_SPAN_ROUND - 1) / HACK_DECODE_SPAN_ROUND * HACK_DECODE_SPAN_ROUND;
   p.chunk = (int)(wg_spans * span);
@@ -986,7 +999,7 @@ DecodePlan plan_decode(const hack_kv_layout& lay, int batch, int num_q_heads, in
 
 template <int BITS, int PI, int GT, int MODE>
 static hipError_t decode_impl(const DecodeArgs& a, int batch, hipStream_t stream) {
-  dim3 grid((unsigned)a.splits, (unsigned)a.c.kv_heads, (unsigned)batch);
+  dim3 grid((unsigned)a.c.kv_heads, (unsigned)batch, (unsigned)a.splits);
   hipLaunchKernelGGL((decode_kernel<BITS, PI, GT, MODE>), grid, dim3(256), 0, stream, a);
   if (MODE == MODE_ATTEND && a.splits > 1 && !HACK_DECODE_FUSED_MERGE)
     hipLaunchKernelGGL(decode_merge_kernel, dim3((unsigned)a.c.kv_heads, (unsigned)batch), dim3(256), 0, stream, a);

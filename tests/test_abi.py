@@ -130,6 +130,9 @@ def test_argument_errors_before_launch(lib):
     lay128 = hk.hack_kv_layout_make(128, 2, 2, 128, 128)
     assert lib.hack_attend_prefill(ctypes.byref(lay128), C, p, 8, 2, 100, 1, p, None) == 2
     assert lib.hack_attend_prefill(L, C, p, 8, 2, 129, 1, p, None) == 3
+    # a sequence per grid row/plane: batch is bounded by the grid's y/z extent
+    assert lib.hack_attend_decode(L, C, p, 8, p, 65536, 100, 0, p, p, 10 ** 12, None) == 2
+    assert lib.hack_attend_prefill(L, C, p, 8, 65536, 100, 1, p, None) == 2
     # decode step: capacity counts the appended token, length arrays must differ,
     # workspace is sized for max_len + 1, paged caches need pages of 4 * partition
     p2 = ctypes.c_void_p(0x6000)
@@ -155,6 +158,10 @@ def test_workspace_grows_with_context(lib):
     b = hk.hack_decode_workspace_bytes(lay, 16, 32, 131072)
     assert 0 < a <= b
     assert hk.hack_decode_workspace_bytes(lay, 16, 31, 4096) == -1
+    # chunk records: at most 65535 chunks per sequence (the grid's z extent),
+    # each holding max, sum and O per query head
+    big = hk.hack_decode_workspace_bytes(lay, 1, 32, 2 ** 31 - 1)
+    assert 0 < big <= 8 * 65535 * 4 * (4 + 128) * 4 + 4096
 
 
 def test_status_strings(lib):
