@@ -50,6 +50,26 @@ def append_bytes(B: int, H: int, d: int, bits: int, pi: int, sum_bytes: int, T_a
     return B * H * per
 
 
+def quantize_bytes(B: int, H: int, L: int, d: int, bits: int, pi: int, sum_bytes: int) -> int:
+    """Bytes one hack_quantize moves: fp16 K and V read once, the compressed cache
+    (K rows, full V blocks, the fp16 open block) written once."""
+    return B * H * (2 * L * d * 2 + decode_bytes_per_seq_head(L, d, bits, pi, sum_bytes))
+
+
+def time_quantize(hk, lay, cache, k, v, lens, L, iters: int = 5):
+    """Median duration (ms) of hack_quantize on the current stream, HIP events around each call."""
+    import torch
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ts = []
+    for _ in range(iters):
+        e0.record()
+        hk.hack_quantize(lay, cache, k, v, lens, L)
+        e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    return float(np.median(ts))
+
+
 def profiled_traffic(kernel_file: str, summary: str):
     """HBM bytes per launch from the committed rocprofv3 counter summary, or None when
     the kernel source has changed since the counters were taken."""
@@ -173,9 +193,12 @@ def main():
                 c.buffers[name].copy_(caches[0].buffers[name])
         caches.append(c)
         lens.append(ln)
+    sb = lay.sum_bytes
+    # quantize-on-write of the whole prompt (the prefill side's output), same cache
+    q_ms = time_quantize(hk, lay, caches[0], k, v, lens[0], L0)
+    q_gbs = quantize_bytes(B, H, L0, d, bits, pi, sb) / (q_ms * 1e-3) / 1e9
     del k, v
     out = torch.empty((B, Hq, d), dtype=torch.float32, device=dev)
-    sb = lay.sum_bytes
 
     # One step = append one token per (sequence, kv head) (quantize-on-write) + decode
     # attention, fused in one launch (hack_decode_step).  The calls are bound once
@@ -244,6 +267,8 @@ def main():
                      "traffic": profiled_traffic("kernels_decode.hip", "decode_llama8b_l4096_hbm_counters.txt"),
                      "avg_kernel_us": round(avg_kern_ms * 1e3, 3),
                      "bytes_per_launch": int(step_bytes)},
+        "quantize": {"workload": "decode_llama8b_l4096 prompt (hack_quantize of 16 x 8 x 4096 tokens)",
+                     "ms": round(q_ms, 4), "GBs": round(q_gbs, 1), "frac_hbm": round(q_gbs / HBM_PEAK_GBS, 4)},
     }
     if not args.no_prefill and args.only is None:
         result["prefill"] = bench_prefill(args.prefill_iters)
@@ -288,9 +313,11 @@ def bench_prefill(iters: int):
         qt.append(e0.elapsed_time(e1))
         at.append(e1.elapsed_time(e2))
     a_ms = float(np.median(at))
+    q_ms = float(np.median(qt))
     tops = ops / (a_ms * 1e-3) / 1e12
+    q_gbs = quantize_bytes(B, H, L, d, wl.kv_bits, wl.partition, lay.sum_bytes) / (q_ms * 1e-3) / 1e9
     return {"workload": "prefill_l8192", "int8_ops": ops, "attend_ms": round(a_ms, 4),
-            "quantize_ms": round(float(np.median(qt)), 4), "TOPS": round(tops, 2),
+            "quantize_ms": round(q_ms, 4), "quantize_GBs": round(q_gbs, 1), "TOPS": round(tops, 2),
             "peak_TOPS": INT8_PEAK_TOPS, "frac": round(tops / INT8_PEAK_TOPS, 4)}
 
 

@@ -1,18 +1,24 @@
-"""Build libhack.so (HIP kernels + C ABI) for gfx950 with hipcc, in-tree."""
+"""Build libhack.so (HIP kernels + C ABI) for gfx950 with hipcc, in-tree.
+
+Each source compiles to its own object in parallel (the kernels of one file never
+call device code of another), then hipcc links the shared library.
+"""
 from __future__ import annotations
 
 import os
 import subprocess
 import sys
+from concurrent.futures import ThreadPoolExecutor
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
+OBJ = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libhack.so")
 SOURCES = ["hack_api.hip", "kernels_quant.hip", "kernels_decode.hip", "kernels_prefill.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
-    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
+    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
     # no packed-fp32 instructions anywhere in the device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     # keep MFMA accumulators in VGPRs: the kernels update them with VALU ops too
@@ -20,19 +26,31 @@ FLAGS = [
     # inputs carry no NaNs (a caller contract): min/max need no quieting of operands
     "-fno-honor-nans",
 ]
+NOISE = "packed-fp32-ops' is not a recognized feature"
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every HIP source into paper_2502_03589_amd/libhack.so; returns its path."""
-    tmp = LIB + ".tmp"
-    cmd = [HIPCC, *FLAGS, "-o", tmp] + [os.path.join(CSRC, s) for s in SOURCES]
+def _run(cmd):
     res = subprocess.run(cmd, capture_output=True, text=True)
-    noise = "packed-fp32-ops' is not a recognized feature"
-    msgs = "\n".join(l for l in (res.stdout + res.stderr).splitlines() if noise not in l)
-    if res.returncode != 0:
-        raise RuntimeError(f"hipcc failed ({res.returncode}):\n{msgs}")
-    if verbose and msgs.strip():
-        print(msgs, file=sys.stderr)
+    msgs = "\n".join(l for l in (res.stdout + res.stderr).splitlines() if NOISE not in l)
+    return res.returncode, msgs
+
+
+def build(verbose: bool = False, extra_flags=()) -> str:
+    """Compile every HIP source and link paper_2502_03589_amd/libhack.so; returns its path."""
+    os.makedirs(OBJ, exist_ok=True)
+    objs = [os.path.join(OBJ, s.replace(".hip", ".o")) for s in SOURCES]
+    cmds = [[HIPCC, *FLAGS, *extra_flags, "-c", "-o", o, os.path.join(CSRC, s)] for s, o in zip(SOURCES, objs)]
+    with ThreadPoolExecutor(max_workers=len(cmds)) as ex:
+        results = list(ex.map(_run, cmds))
+    for (rc, msgs), s in zip(results, SOURCES):
+        if rc != 0:
+            raise RuntimeError(f"hipcc failed on {s} ({rc}):\n{msgs}")
+        if verbose and msgs.strip():
+            print(msgs, file=sys.stderr)
+    tmp = LIB + ".tmp"
+    rc, msgs = _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs])
+    if rc != 0:
+        raise RuntimeError(f"hipcc link failed ({rc}):\n{msgs}")
     os.replace(tmp, LIB)
     return LIB
 

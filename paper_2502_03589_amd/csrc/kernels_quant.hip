@@ -1,9 +1,11 @@
 // Quantize-on-write kernels (Sec. 5.1 steps 2 and 9; Sec. 5.2 quantizer; Sec. 5.3
 // partitioning and the fp16 open V block).
 //   quantize_k: one thread per (sequence, kv head, token, K partition along d)
-//   quantize_v: one thread per (sequence, kv head, V block, channel)
+//   quantize_v: one thread per (sequence, kv head, V block, channel pair)
 //   append    : one workgroup per sequence, one new token for every kv head
 // All are HBM-bound: they read fp16 values once and write codes, (min, scale) and sums.
+#include <type_traits>
+
 #include "hack_internal.hpp"
 
 namespace hack {
@@ -35,17 +37,22 @@ __global__ __launch_bounds__(256) void quantize_k_kernel(CacheView c, const __ha
   store_sum(c.k_sums, row * P + p, c.sum_bytes, sum);
 }
 
+// V: one thread per (sequence, kv head, V block, channel pair).  The threads of a
+// block's channel pairs are consecutive, so each of the block's PI token rows is
+// read as one contiguous run of 4-byte loads (a whole row per 64 pairs), and each
+// thread writes the adjacent codes, (min, scale) and sums of its two channels.
 template <int BITS, int PI>
 __global__ __launch_bounds__(256) void quantize_v_kernel(CacheView c, const __half* __restrict__ v,
                                                          const int32_t* __restrict__ lens, int batch,
                                                          int max_len, int stochastic, uint64_t key) {
-  const int d = c.head_dim;
+  constexpr int CB = PI * BITS / 8;  // code bytes per (block, channel)
+  const int d = c.head_dim, pairs = d / 2;
   const int NB = (max_len + PI - 1) / PI;
-  const int64_t total = (int64_t)batch * c.kv_heads * NB * d;
+  const int64_t total = (int64_t)batch * c.kv_heads * NB * pairs;
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (gid >= total) return;
-  const int ch = (int)(gid % d);
-  int64_t r = gid / d;
+  const int ch = 2 * (int)(gid % pairs);
+  int64_t r = gid / pairs;
   const int blk = (int)(r % NB);
   r /= NB;
   const int h = (int)(r % c.kv_heads);
@@ -55,20 +62,53 @@ __global__ __launch_bounds__(256) void quantize_v_kernel(CacheView c, const __ha
   if (blk > F || (blk == F && T == 0)) return;
   const int n = blk < F ? PI : T;
   const __half* src = v + (((int64_t)s * c.kv_heads + h) * max_len + (int64_t)blk * PI) * d + ch;
-  float x[PI];
+  uint32_t raw[PI];  // (channel ch, channel ch + 1) of each token row
 #pragma unroll
-  for (int e = 0; e < PI; ++e) x[e] = e < n ? __half2float(src[(int64_t)e * d]) : 0.0f;
-  uint32_t w[(PI * BITS + 31) / 32];
-  uint16_t mb, sb;
-  const uint32_t sum = quantize_values<BITS, PI>(
-      x, n, stochastic != 0, key, element_index(s, c.kv_heads, h, blk * PI, d, ch), (uint64_t)d, w, mb, sb);
+  for (int e = 0; e < PI; ++e) raw[e] = e < n ? *reinterpret_cast<const uint32_t*>(src + (int64_t)e * d) : 0u;
   const int64_t vb = v_block<PI>(c, s, h, blk * PI);
-  store_codes<BITS, PI>(c.v_codes + (vb * d + ch) * (PI * BITS / 8), w);
-  reinterpret_cast<uint32_t*>(c.v_meta)[vb * d + ch] = (uint32_t)mb | ((uint32_t)sb << 16);
-  store_sum(c.v_sums, vb * d + ch, c.sum_bytes, sum);
+  constexpr int NW = (PI * BITS + 31) / 32;
+  uint32_t meta[2], sums[2];
+  uint32_t w0[NW], w1[NW];
+  // channel ch + j of the pair: the half j of every raw word
+  auto quantize_channel = [&](auto j_tag, uint32_t (&w)[NW]) __attribute__((always_inline)) {
+    constexpr int J = decltype(j_tag)::value;
+    float x[PI];
+#pragma unroll
+    for (int e = 0; e < PI; ++e) x[e] = __half2float(__ushort_as_half((uint16_t)(raw[e] >> (16 * J))));
+    uint16_t mb, sb;
+    sums[J] = quantize_values<BITS, PI>(x, n, stochastic != 0, key,
+                                        element_index(s, c.kv_heads, h, blk * PI, d, ch + J), (uint64_t)d, w, mb,
+                                        sb);
+    meta[J] = (uint32_t)mb | ((uint32_t)sb << 16);
+  };
+  quantize_channel(std::integral_constant<int, 0>{}, w0);
+  quantize_channel(std::integral_constant<int, 1>{}, w1);
+  // the two channels' codes are adjacent: 2 * CB bytes from a 2 * CB-aligned offset
+  uint32_t both[2 * NW];
+#pragma unroll
+  for (int i = 0; i < NW; ++i) {
+    both[i] = w0[i];
+    both[NW + i] = w1[i];
+  }
+  uint8_t* cdst = c.v_codes + (vb * d + ch) * CB;
+  if constexpr (2 * CB % 16 == 0) {
+#pragma unroll
+    for (int i = 0; i < 2 * CB / 16; ++i)
+      reinterpret_cast<uint4*>(cdst)[i] = uint4{both[4 * i], both[4 * i + 1], both[4 * i + 2], both[4 * i + 3]};
+  } else {
+    *reinterpret_cast<uint2*>(cdst) = uint2{both[0], both[1]};
+  }
+  *reinterpret_cast<uint2*>(reinterpret_cast<uint32_t*>(c.v_meta) + vb * d + ch) = uint2{meta[0], meta[1]};
+  if (c.sum_bytes == 1) {
+    *reinterpret_cast<uint16_t*>(c.v_sums + vb * d + ch) = (uint16_t)(sums[0] | (sums[1] << 8));
+  } else {
+    *reinterpret_cast<uint32_t*>(c.v_sums + 2 * (vb * d + ch)) = sums[0] | (sums[1] << 16);
+  }
   if (blk == F) {  // the open block: keep its fp16 originals
     __half* tail = c.v_tail + (((int64_t)s * c.kv_heads + h) * PI) * d + ch;
-    for (int e = 0; e < T; ++e) tail[(int64_t)e * d] = src[(int64_t)e * d];
+#pragma unroll
+    for (int e = 0; e < PI; ++e)
+      if (e < T) *reinterpret_cast<uint32_t*>(tail + (int64_t)e * d) = raw[e];
   }
 }
 
@@ -154,7 +194,7 @@ static hipError_t quantize_impl(const hack_kv_layout& lay, const CacheView& c, c
   if (nk > 0)
     hipLaunchKernelGGL((quantize_k_kernel<BITS, PI>), dim3((unsigned)((nk + 255) / 256)), dim3(256), 0,
                        stream, c, k, lens, batch, max_len, stoch, stream_key(lay.seed, 1));
-  const int64_t nv = (int64_t)batch * c.kv_heads * ((max_len + PI - 1) / PI) * c.head_dim;
+  const int64_t nv = (int64_t)batch * c.kv_heads * ((max_len + PI - 1) / PI) * (c.head_dim / 2);
   if (nv > 0)
     hipLaunchKernelGGL((quantize_v_kernel<BITS, PI>), dim3((unsigned)((nv + 255) / 256)), dim3(256), 0,
                        stream, c, v, lens, batch, max_len, stoch, stream_key(lay.seed, 2));
