@@ -272,22 +272,24 @@ def main():
     }
     if not args.no_prefill and args.only is None:
         result["prefill"] = bench_prefill(args.prefill_iters)
+        # the same workload with 4-bit Q/P codes (the literal reading of its 4-bit Q/K/V/P)
+        result["prefill_qp4"] = bench_prefill(max(3, args.prefill_iters // 2), 4)
     if not args.no_cpu_baseline and args.only is None:
         result["cpu_baseline"] = cpu_baseline_decode(wl)
     print(json.dumps(result), flush=True)
 
 
-def bench_prefill(iters: int):
-    """Causal prefill (batch 1, 32/8 heads, 8192 tokens, 4-bit K/V, partition 64):
-    quantize-on-write of the prompt's K/V then attention; int8 ops of the causal
-    triangle = 2 products x 32 heads x L(L+1)/2 x 128 x 2."""
+def bench_prefill(iters: int, qp_bits: int = 8):
+    """Causal prefill (batch 1, 32/8 heads, 8192 tokens, 4-bit K/V, partition 64, Q/P
+    codes of qp_bits bits): quantize-on-write of the prompt's K/V then attention; int8
+    ops of the causal triangle = 2 products x 32 heads x L(L+1)/2 x 128 x 2."""
     import torch
     from paper_2502_03589_amd import hack as hk
     from paper_2502_03589_amd import synth
     wl = synth.WORKLOADS["prefill_l8192"]
     B, Hq, H, d, L = wl.batch, wl.q_heads, wl.kv_heads, wl.head_dim, wl.context
     dev = torch.device("cuda:0")
-    lay = hk.hack_kv_layout_make(d, H, wl.kv_bits, wl.partition, L)
+    lay = hk.hack_kv_layout_make(d, H, wl.kv_bits, wl.partition, L, qp_bits)
     c = hk.KVCache(lay, B, B, None, dev)
     k = torch.from_numpy(synth.normal_f16(wl.seed, "k", (B, H, L, d))).to(dev)
     v = torch.from_numpy(synth.normal_f16(wl.seed, "v", (B, H, L, d))).to(dev)
@@ -316,7 +318,7 @@ def bench_prefill(iters: int):
     q_ms = float(np.median(qt))
     tops = ops / (a_ms * 1e-3) / 1e12
     q_gbs = quantize_bytes(B, H, L, d, wl.kv_bits, wl.partition, lay.sum_bytes) / (q_ms * 1e-3) / 1e9
-    return {"workload": "prefill_l8192", "int8_ops": ops, "attend_ms": round(a_ms, 4),
+    return {"workload": "prefill_l8192", "qp_bits": qp_bits, "int8_ops": ops, "attend_ms": round(a_ms, 4),
             "quantize_ms": round(q_ms, 4), "quantize_GBs": round(q_gbs, 1), "TOPS": round(tops, 2),
             "peak_TOPS": INT8_PEAK_TOPS, "frac": round(tops / INT8_PEAK_TOPS, 4)}
 

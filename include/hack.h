@@ -85,7 +85,8 @@ typedef struct hack_kv_layout {
   int32_t kv_bits;       /* b, bits per stored K/V code: 2 or 4                    */
   int32_t partition;     /* Pi: 16, 32, 64 or 128 (a multiple of 16, Sec. 5.3)     */
   int32_t page_tokens;   /* tokens per page; a multiple of Pi                      */
-  int32_t qp_bits;       /* bits of the transient Q and P codes: 8 (Sec. 5.1)      */
+  int32_t qp_bits;       /* bits of the transient Q and P codes: 8 (Sec. 5.1, the
+                            paper's INT8) or 4                                      */
   int32_t rounding;      /* HACK_ROUND_*                                           */
   int32_t sum_bytes;     /* 1 if b + ceil(log2 Pi) <= 8 else 2 (Sec. 5.3, Sec. 6)  */
   uint64_t seed;         /* stochastic-rounding seed                               */
@@ -112,7 +113,7 @@ typedef struct hack_kv_cache {
 /* Fill *out with a validated layout.  Rejects (HACK_ERR_INVALID_ARGUMENT) a null
  * out, head_dim not a positive multiple of partition or above 256, num_kv_heads < 1,
  * kv_bits not in {2,4}, partition not in {16,32,64,128}, page_tokens not a positive
- * multiple of partition, qp_bits != 8, an unknown rounding mode.  Host only. */
+ * multiple of partition, qp_bits not in {4,8}, an unknown rounding mode.  Host only. */
 hack_status hack_kv_layout_make(hack_kv_layout* out, int32_t head_dim, int32_t num_kv_heads,
                                 int32_t kv_bits, int32_t partition, int32_t page_tokens,
                                 int32_t qp_bits, int32_t rounding, uint64_t seed);

@@ -18,7 +18,7 @@ bool layout_ok(const hack_kv_layout* l) {
   if (l->num_kv_heads < 1) return false;
   if (!(l->kv_bits == 2 || l->kv_bits == 4)) return false;
   if (l->page_tokens <= 0 || l->page_tokens % pi != 0) return false;
-  if (l->qp_bits != 8) return false;
+  if (!(l->qp_bits == 8 || l->qp_bits == 4)) return false;
   if (!(l->rounding == HACK_ROUND_NEAREST_EVEN || l->rounding == HACK_ROUND_STOCHASTIC)) return false;
   int need = l->kv_bits;
   for (int v = 1; v < pi; v <<= 1) ++need;  // b + ceil(log2 pi)
@@ -170,6 +170,10 @@ static hack_status decode_common(const hack_kv_layout* layout, const hack_kv_cac
   a.num_q_heads = num_q_heads;
   a.group = num_q_heads / layout->num_kv_heads;
   a.max_len = max_len;
+  a.qmax = (float)((1 << layout->qp_bits) - 1);
+  a.inv_qmax = 1.0f / a.qmax;
+  a.qoff = 1 << (layout->qp_bits - 1);
+  a.qoff_f = (float)a.qoff;
   *cap_out = cap;
   return HACK_OK;
 }

@@ -46,6 +46,10 @@ struct DecodeArgs {
   int splits;
   int tail_requant;
   int max_len;
+  float qmax;             // 2^b_QP - 1 of the transient Q and P codes (15 or 255)
+  float inv_qmax;         // 1 / qmax
+  int qoff;               // Q/P codes enter the signed int8 MFMA as code - qoff, qoff = 2^(b_QP - 1)
+  float qoff_f;
   // fused append (hack_decode_step): when k_new is set, token lens[s] of every
   // (sequence, kv head) is appended first, the attention covers lens[s] + 1 tokens
   // and lens_out[s] = lens[s] + 1

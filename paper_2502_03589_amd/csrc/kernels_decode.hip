@@ -6,7 +6,7 @@
 // is issued before any of its arithmetic, from wave-uniform section bases plus
 // fixed per-lane offsets.  Per span a wave computes, for up to 4 query heads of the
 // kv group per row tile:
-//   Q'K'  v_mfma_i32_16x16x64_i8: A = 8-bit Q codes (minus 128) with rows
+//   Q'K'  v_mfma_i32_16x16x64_i8: A = Q codes minus 2^(b-1) (signed) with rows
 //         (head h, channel quarter q), block-diagonal so that lane group g only
 //         carries quarter g; B = 2/4-bit K codes unpacked in registers (lane = token,
 //         group = quarter).  Lane (t, g) receives the four quarter products of head g.
@@ -232,7 +232,7 @@ constexpr bool decode_v_in_lds() {
 template <int BITS, int PI, int GT>
 struct WaveLds {
   static constexpr int HT = 4 * GT;
-  int8_t p[GT][4][4][PI];       // P codes - 128: [row tile][block][head][token position]
+  int8_t p[GT][4][4][PI];       // P codes - qoff: [row tile][block][head][token position]
   float pst[GT][4][2][4];       // [rt][block][s_p | m~_p][head], scaled to the span's reference max
   float alpha[GT][4];           // O rescale of the span, per head
   float tailf[GT][4];           // scale of the fp16 open block's probabilities
@@ -338,7 +338,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
   constexpr int HT = GT * 4;
   constexpr int KROW = D * BITS / 8; // K code bytes per token
 
-  // Q codes - 128 per (head slot, quarter, 16-channel slice), each slice already in
+  // Q codes - qoff per (head slot, quarter, 16-channel slice), each slice already in
   // the byte order of the K operand's in-register unpack
   __shared__ __attribute__((aligned(16))) int8_t q_lds[HT][4][2][16];
   __shared__ float qm_lds[HT][4][3];
@@ -358,6 +358,16 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
   const int G = a.group, Hq = a.num_q_heads, H = c.kv_heads;
   // lengths outside [0, max_len] break the caller contract; clamp so that every
   // access stays inside the cache and the workspace
+  // this wave's query values (head slots wave, wave + 4, ...) do not depend on the
+  // length: their loads are issued first so the two memory round trips overlap
+  uint32_t qraw[GT];
+#pragma unroll
+  for (int i = 0; i < GT; ++i) {
+    const int gh = wave + kWaves * i;
+    qraw[i] = (MODE != MODE_PV && gh < G)
+                  ? reinterpret_cast<const uint32_t*>(a.q + ((int64_t)s * Hq + hkv * G + gh) * D)[lane]
+                  : 0u;
+  }
   const int Lin = a.lens[s];
   int Lq = max(0, min(Lin, a.max_len));
   const int t0 = split * a.chunk;
@@ -391,12 +401,14 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
   // ---- Q: 8-bit codes per partition with float32 metadata (Sec. 5.1, Sec. 5.2) ----
   // wave w quantizes head slots w, w+4, ...; each lane holds two channels
   if constexpr (MODE != MODE_PV) {
-    for (int gh = wave; gh < HT; gh += kWaves) {
+#pragma unroll
+    for (int i = 0; i < GT; ++i) {
+      const int gh = wave + kWaves * i;
       const bool real = gh < G;
       const int hq = hkv * G + gh;
       float x0 = 0.0f, x1 = 0.0f;
       if (real) {
-        const float2 f = __half22float2(reinterpret_cast<const __half2*>(a.q + ((int64_t)s * Hq + hq) * D)[lane]);
+        const float2 f = __half22float2(*reinterpret_cast<const __half2*>(&qraw[i]));
         x0 = f.x;
         x1 = f.y;
       }
@@ -409,11 +421,11 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
       float sq, c0 = 0.0f, c1 = 0.0f;
       {
 #pragma clang fp contract(off)
-        sq = __fdiv_rn(__fsub_rn(mx, mn), 255.0f);
+        sq = __fdiv_rn(__fsub_rn(mx, mn), a.qmax);
         if (sq != 0.0f) {
           const float r = __fdiv_rn(1.0f, sq);
-          c0 = fminf(rintf(__fmul_rn(__fsub_rn(x0, mn), r)), 255.0f);
-          c1 = fminf(rintf(__fmul_rn(__fsub_rn(x1, mn), r)), 255.0f);
+          c0 = fminf(rintf(__fmul_rn(__fsub_rn(x0, mn), r)), a.qmax);
+          c1 = fminf(rintf(__fmul_rn(__fsub_rn(x1, mn), r)), a.qmax);
         }
       }
       int csum = (int)c0 + (int)c1;
@@ -422,14 +434,14 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
       {
         const int ch = 2 * lane;  // channels ch, ch + 1 share quarter and slice
         const int g = ch >> 5, m = (ch >> 4) & 1, e = ch & 15;
-        q_lds[gh][g][m][perm_position<BITS>(e)] = real ? (int8_t)((int)c0 - 128) : (int8_t)0;
-        q_lds[gh][g][m][perm_position<BITS>(e + 1)] = real ? (int8_t)((int)c1 - 128) : (int8_t)0;
+        q_lds[gh][g][m][perm_position<BITS>(e)] = real ? (int8_t)((int)c0 - a.qoff) : (int8_t)0;
+        q_lds[gh][g][m][perm_position<BITS>(e + 1)] = real ? (int8_t)((int)c1 - a.qoff) : (int8_t)0;
       }
       const int p = (2 * lane) / PI;
       if ((2 * lane) % PI == 0) {
-        // per partition: s_q, m~_q = m_q + 128 s_q, R = s_q sum q' + n m_q (all in log2 units)
+        // per partition: s_q, m~_q = m_q + qoff s_q, R = s_q sum q' + n m_q (all in log2 units)
         qm_lds[gh][p][0] = real ? kScoreScale * sq : 0.0f;
-        qm_lds[gh][p][1] = real ? kScoreScale * (mn + 128.0f * sq) : 0.0f;
+        qm_lds[gh][p][1] = real ? kScoreScale * (mn + a.qoff_f * sq) : 0.0f;
         qm_lds[gh][p][2] = real ? kScoreScale * (sq * (float)csum + (float)PI * mn) : 0.0f;
         if (MODE == MODE_QK && real && split == 0) {
           a.dbg_qmeta[(((int64_t)s * Hq + hq) * P + p) * 2 + 0] = mn;
@@ -581,7 +593,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
           const int gh = rt * 4 + hh;
           int8_t v = 0;
           if (present && kb < F && gh < G)
-            v = (int8_t)((int)a.dbg_pcodes[(((int64_t)s * Hq + hkv * G + gh) * NB + kb) * PI + e] ^ 0x80);
+            v = (int8_t)((int)a.dbg_pcodes[(((int64_t)s * Hq + hkv * G + gh) * NB + kb) * PI + e] - a.qoff);
           wl.p[rt][k][hh][(e >> 4) * 16 + perm_position<BITS>(e & 15)] = v;
         }
         if (lane < HT) {
@@ -593,7 +605,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
             ps = a.dbg_pmeta[base * 2 + 1];
           }
           wl.pst[rt][k][0][hh] = ps;
-          wl.pst[rt][k][1][hh] = pm + 128.0f * ps;
+          wl.pst[rt][k][1][hh] = pm + a.qoff_f * ps;
         }
         continue;
       } else {
@@ -633,7 +645,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
               if (tok < L && gh < G) {
 #pragma unroll
                 for (int p = 0; p < P; ++p) {
-                  int v = 128 * zq[p];
+                  int v = a.qoff * zq[p];
 #pragma unroll
                   for (int q = p * QPP; q < (p + 1) * QPP; ++q) v += acc[q];
                   a.dbg_prod[(((int64_t)s * Hq + hkv * G + gh) * a.max_len + tok) * P + p] = v;
@@ -673,16 +685,16 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
             const float pmax = __builtin_amdgcn_exp2f(bmax - mr);
             const float pmin = __builtin_amdgcn_exp2f(bmin - mr);
             const float dp = pmax - pmin;
-            const float r = dp > 0.0f ? 255.0f * __builtin_amdgcn_rcpf(dp) : 0.0f;
+            const float r = dp > 0.0f ? a.qmax * __builtin_amdgcn_rcpf(dp) : 0.0f;
             const float bias = -pmin * r;
 #pragma unroll
             for (int tl = 0; tl < TILES; ++tl) {
-              // round-to-nearest-even with saturation to [0, 255]
+              // round-to-nearest-even with saturation (codes stay within [0, qmax])
               const uint32_t code = __builtin_amdgcn_cvt_pk_u8_f32(fmaf(pt[tl], r, bias), 0, 0u);
               const bool valid = full || bt0 + 16 * tl + col < L;
-              wl.p[rt][k][grp][tl * 16 + perm_position<BITS>(col)] = valid ? (int8_t)(code ^ 0x80u) : (int8_t)0;
+              wl.p[rt][k][grp][tl * 16 + perm_position<BITS>(col)] = valid ? (int8_t)((int)code - a.qoff) : (int8_t)0;
             }
-            ps_s[rt][k] = dp * (1.0f / 255.0f);
+            ps_s[rt][k] = dp * a.inv_qmax;
             ps_m[rt][k] = pmin;
           } else {
 #pragma unroll
@@ -704,7 +716,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
           for (int k = 0; k < 4; ++k) {
             const float f = __builtin_amdgcn_exp2f(m_blk[rt][k] - m_ref[rt]);
             wl.pst[rt][k][0][grp] = ps_s[rt][k] * f;
-            wl.pst[rt][k][1][grp] = (ps_m[rt][k] + 128.0f * ps_s[rt][k]) * f;
+            wl.pst[rt][k][1][grp] = (ps_m[rt][k] + a.qoff_f * ps_s[rt][k]) * f;
             if (k == kF) wl.tailf[rt][grp] = f;
           }
           wl.alpha[rt][grp] = __builtin_amdgcn_exp2f(m_start[rt] - m_ref[rt]);
@@ -782,7 +794,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
         // (such a lane's own registers hold the sums of block g = kk)
         pr0[rt] = kk == grp ? wl.pst[rt][kk][0][hh] : 0.0f;                  // s_p
         pr1[rt] = pr0[rt] * pick4(zp, hh);                                   // s_p * sum p~'
-        pr2[rt] = kk == grp ? wl.pst[rt][kk][1][hh] : 0.0f;                 // m~_p = m_p + 128 s_p
+        pr2[rt] = kk == grp ? wl.pst[rt][kk][1][hh] : 0.0f;                 // m~_p = m_p + qoff s_p
       }
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
@@ -809,7 +821,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
               const int gh = rt * 4 + i;
               if (gvalid && gh < G)
                 a.dbg_prod[(((int64_t)s * Hq + hkv * G + gh) * (a.max_len / PI) + vkb) * D + 8 * col + j] =
-                    acc[i] + 128 * (int)zj;
+                    acc[i] + a.qoff * (int)zj;
             }
           }
         }

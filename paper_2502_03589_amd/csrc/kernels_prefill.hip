@@ -9,7 +9,7 @@
 //            per-token K and per-channel V metadata) into the other LDS buffer while
 //            the waves compute block kb.
 //   S^T = K'Q'^T  v_mfma_i32_16x16{32,64}_i8, one per (16-token tile, 16-row tile,
-//            K partition): A = K codes (lane = token), B = 8-bit Q codes minus 128
+//            K partition): A = K codes (lane = token), B = Q codes minus 2^(b-1)
 //            quantized in registers (lane = query row).  Lane (row n, group g) gets
 //            tokens 4g..4g+3 of the tile for row n.  Eq. 4: the rank-1 terms
 //            (m~_q s_k sum k' + R m_k, all partitions) are outer products of a
@@ -25,6 +25,8 @@
 //   O^T = V'^T P'^T  one MFMA per (16-channel tile, row tile); an all-ones A gives
 //            the P code sums; Eq. 4 with the cached V sums on the VALU.
 //   open block  (len mod PI tokens) multiplied in fp16 with unquantized p.
+#include <type_traits>
+
 #include "hack_internal.hpp"
 
 namespace hack {
@@ -145,6 +147,10 @@ struct PrefillArgs {
   int len;
   int causal;
   int nqb;           // query blocks of kRows rows
+  float qmax;        // 2^b_QP - 1 of the transient Q and P codes (15 or 255)
+  float inv_qmax;    // 1 / qmax
+  int qoff;          // Q/P codes enter the signed int8 MFMA as code - qoff, qoff = 2^(b_QP - 1)
+  float qoff_f;
 };
 
 // Staging of one V block by the 512 threads of the workgroup (threads 0-255: K,
@@ -158,10 +164,20 @@ struct StageRegs {
   uint32_t meta, sum; // K metadata of (token, partition) or V metadata of a channel
 };
 
+// Bytes of one cached code sum: 1 when b + log2(PI) <= 8, else 2 (Sec. 5.3).
+template <int BITS, int PI>
+constexpr int sum_bytes() {
+  int need = BITS;
+  for (int v = 1; v < PI; v <<= 1) ++need;
+  return need <= 8 ? 1 : 2;
+}
+
+// Section bases of the block are wave-uniform; each thread adds a 32-bit offset
+// that is recomputed from its index (not kept live across the block loop).
 template <int BITS, int PI>
 __device__ __forceinline__ void stage_load(const PrefillArgs& a, StageRegs<BITS, PI>& r, int s, int hkv, int kb,
                                            bool with_v) {
-  constexpr int D = 128, P = PrefillCfg<PI>::P;
+  constexpr int D = 128, P = PrefillCfg<PI>::P, SB = sum_bytes<BITS, PI>();
   constexpr int CPT = PI / 2, TPR = D / CPT;
   const CacheView& c = a.c;
   const int tid = threadIdx.x;
@@ -173,27 +189,35 @@ __device__ __forceinline__ void stage_load(const PrefillArgs& a, StageRegs<BITS,
   for (int i = 0; i < StageRegs<BITS, PI>::KW; ++i) r.w[i] = 0u;
   if (tid < 256) {
     // K codes: thread -> (token tid / TPR, PI/2 channels)
-    const int tt = tid / TPR, cb = (tid % TPR) * CPT;
-    const uint32_t* src = reinterpret_cast<const uint32_t*>(c.k_codes + (krow0 + tt) * (D * BITS / 8) + cb * BITS / 8);
+    const uint8_t* kc = c.k_codes + krow0 * (D * BITS / 8);
+    uint32_t off = (uint32_t)((tid / TPR) * (D * BITS / 8) + (tid % TPR) * CPT * BITS / 8);
+    asm volatile("" : "+v"(off));
+    const uint32_t* src = reinterpret_cast<const uint32_t*>(kc + off);
 #pragma unroll
     for (int i = 0; i < StageRegs<BITS, PI>::KW; ++i) r.w[i] = src[i];
-    if (tid < PI * P) {  // K metadata: thread -> (token, partition)
-      const int64_t mi = (krow0 + tid / P) * P + tid % P;
-      r.meta = reinterpret_cast<const uint32_t*>(c.k_meta)[mi];
-      r.sum = load_sum(c.k_sums, mi, c.sum_bytes);
+    if (tid < PI * P) {  // K metadata: thread -> (token, partition); rows of P entries
+      uint32_t mi = (uint32_t)tid;
+      asm volatile("" : "+v"(mi));
+      r.meta = reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(c.k_meta) + krow0 * P * 4)[mi];
+      const uint8_t* ks = c.k_sums + krow0 * P * SB;
+      r.sum = SB == 1 ? (uint32_t)ks[mi] : (uint32_t)reinterpret_cast<const uint16_t*>(ks)[mi];
     }
   } else if (with_v) {
     const int64_t vb = (page * c.kv_heads + hkv) * (c.page_tokens / PI) + ((int64_t)(kb * PI) % c.page_tokens) / PI;
     const int vt = tid - 256;
     // V codes: two threads per channel, PI/2 tokens each
-    const int ch = vt >> 1, half = vt & 1;
-    const uint32_t* src = reinterpret_cast<const uint32_t*>(c.v_codes + (vb * D + ch) * (PI * BITS / 8) +
-                                                            half * (PI / 2) * BITS / 8);
+    const uint8_t* vc = c.v_codes + vb * D * (PI * BITS / 8);
+    uint32_t off = (uint32_t)((vt >> 1) * (PI * BITS / 8) + (vt & 1) * (PI / 2) * BITS / 8);
+    asm volatile("" : "+v"(off));
+    const uint32_t* src = reinterpret_cast<const uint32_t*>(vc + off);
 #pragma unroll
     for (int i = 0; i < StageRegs<BITS, PI>::KW; ++i) r.w[i] = src[i];
     if (vt < D) {
-      r.meta = reinterpret_cast<const uint32_t*>(c.v_meta)[vb * D + vt];
-      r.sum = load_sum(c.v_sums, vb * D + vt, c.sum_bytes);
+      uint32_t mi = (uint32_t)vt;
+      asm volatile("" : "+v"(mi));
+      r.meta = reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(c.v_meta) + vb * D * 4)[mi];
+      const uint8_t* vs = c.v_sums + vb * D * SB;
+      r.sum = SB == 1 ? (uint32_t)vs[mi] : (uint32_t)reinterpret_cast<const uint16_t*>(vs)[mi];
     }
   }
 }
@@ -330,7 +354,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
       float s32;
       {
 #pragma clang fp contract(off)
-        s32 = __fdiv_rn(__fsub_rn(mx, mn), 255.0f);
+        s32 = __fdiv_rn(__fsub_rn(mx, mn), a.qmax);
         const float r = s32 != 0.0f ? __fdiv_rn(1.0f, s32) : 0.0f;
 #pragma unroll
         for (int e4 = 0; e4 < KSL / 4; ++e4) {
@@ -338,18 +362,18 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const float t = __fmul_rn(__fsub_rn(x[4 * e4 + i], mn), r);
-            const int code = s32 != 0.0f ? (int)fminf(rintf(t), 255.0f) : 0;
+            const int code = s32 != 0.0f ? (int)fminf(rintf(t), a.qmax) : 0;
             csum += code;
-            v |= (uint32_t)(code ^ 0x80) << (8 * i);
+            v |= (uint32_t)((code - a.qoff) & 0xFF) << (8 * i);
           }
           w[e4] = v;
         }
       }
       csum = xg_sum_i(csum);
       qop[p] = OP::from(w);
-      // Eq. 4 coefficients in log2 units: s_q, m~_q = m_q + 128 s_q, R = s_q sum q' + n m_q
+      // Eq. 4 coefficients in log2 units: s_q, m~_q = m_q + qoff s_q, R = s_q sum q' + n m_q
       sq[p] = kScale * s32;
-      mq[p] = kScale * (mn + 128.0f * s32);
+      mq[p] = kScale * (mn + a.qoff_f * s32);
       rq[p] = kScale * (s32 * (float)csum + (float)PI * mn);
     }
   }
@@ -393,17 +417,19 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
   }
   __syncthreads();
 
-  for (int kb = 0; kb < nblk; ++kb) {
+  // One V block: quantized blocks run in the main loop; the fp16 open block (at most
+  // one, the last) runs after it, so the loop body holds no branch on the block kind.
+  auto block = [&](const int kb, auto tail_tag) __attribute__((always_inline)) {
+    constexpr bool is_tail = decltype(tail_tag)::value;  // the fp16 open block
     Stage<PI>& st = stages[kb & 1];
     const VMeta& vmc = vm_ring[kb % 3];
     const bool next = kb + 1 < nblk;
     if (next) stage_load<BITS, PI>(a, sr, s, hkv, kb + 1, kb + 1 < F);
-    const bool is_tail = kb >= F;  // the fp16 open block
     const int tb0 = kb * PI;
 
     // ---------------- S^T tiles and Eq. 4 (lane: row `row`, tokens 16 tl + 4 grp + i) ----------------
     // masking is needed only in the block holding the length or this wave's diagonal
-    const bool need_mask = tb0 + PI > L || (a.causal && tb0 + PI - 1 > r0 + 16 * (wave >> 2));
+    const bool need_mask = is_tail || tb0 + PI > L || (a.causal && tb0 + PI - 1 > r0 + 16 * (wave >> 2));
     float sv[TL][4];
 #pragma unroll
     for (int tl = 0; tl < TL; ++tl) {
@@ -486,23 +512,25 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
       }
     l_run += lsum;
 
-    if (!is_tail) {
+    if constexpr (!is_tail) {
       pmin = xg_min(pmin);
       const float pmax = bmax > -INFINITY ? __builtin_amdgcn_exp2f(bmax - m_ref) : 0.0f;
       const float dp = pmax - pmin;
-      const float r = dp > 0.0f ? 255.0f * __builtin_amdgcn_rcpf(dp) : 0.0f;
-      const float bias = -pmin * r;
+      const float r = dp > 0.0f ? a.qmax * __builtin_amdgcn_rcpf(dp) : 0.0f;
+      // bytes code + 128 - qoff (an integer shift before rounding changes no code),
+      // then bit 7 flipped: code - qoff as a signed byte
+      const float bias = fmaf(-pmin, r, 128.0f - a.qoff_f);
       uint32_t w[TL];
 #pragma unroll
       for (int tl = 0; tl < TL; ++tl) {
         uint32_t v = 0;
 #pragma unroll
         for (int i = 0; i < 4; ++i) v = __builtin_amdgcn_cvt_pk_u8_f32(fmaf(pt[tl][i], r, bias), i, v);
-        w[tl] = v ^ 0x80808080u;  // codes - 128
+        w[tl] = v ^ 0x80808080u;
       }
       const opT pop = OP::from(w);
-      const float ps = dp * (1.0f / 255.0f);   // s_p
-      const float pm = pmin + 128.0f * ps;     // m~_p
+      const float ps = dp * a.inv_qmax;        // s_p
+      const float pm = pmin + a.qoff_f * ps;   // m~_p
       // sum of the signed codes of this row's block: all-ones A operand
       const v4i z = OP::mfma(OP::ones(), pop, v4i{0, 0, 0, 0});
       const float pz = ps * (float)z[0];       // s_p * sum p~'
@@ -580,7 +608,10 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
     }
     if (next) stage_store<BITS, PI>(sr, stages[(kb + 1) & 1], vm_ring[(kb + 1) % 3], kb + 1 < F);
     __syncthreads();  // stage kb+1 complete; stage kb free for kb+2
-  }
+  };
+  const int nq = min(nblk, F);
+  for (int kb = 0; kb < nq; ++kb) block(kb, std::false_type{});
+  if (nblk > nq) block(nq, std::true_type{});
 
 #if HACK_PREFILL_PV_RANK_PAIRED
   if (rk_blk >= 0) rank_pair(vm_ring[0], 0.0f, 0.0f, false);
@@ -616,6 +647,10 @@ hipError_t launch_prefill(const hack_kv_layout& lay, const CacheView& c, const _
   a.len = len;
   a.causal = causal;
   a.nqb = (len + kRows - 1) / kRows;
+  a.qmax = (float)((1 << lay.qp_bits) - 1);
+  a.inv_qmax = 1.0f / a.qmax;
+  a.qoff = 1 << (lay.qp_bits - 1);
+  a.qoff_f = (float)a.qoff;
   switch (lay.kv_bits * 1000 + lay.partition) {
     case 2032: return prefill_impl<2, 32>(a, batch, stream);
     case 2064: return prefill_impl<2, 64>(a, batch, stream);

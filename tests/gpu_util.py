@@ -23,7 +23,7 @@ class Case:
     """K/V/q inputs, a device cache written by hack_quantize, and the oracle's sequences."""
 
     def __init__(self, seed, batch, kv_heads, lens, bits, pi, group=4, d=128, paged_page=0,
-                 rounding=O.NEAREST_EVEN, spare_tokens=0, outliers=0):
+                 rounding=O.NEAREST_EVEN, spare_tokens=0, outliers=0, qp_bits=8):
         self.seed, self.batch, self.H, self.d = seed, batch, kv_heads, d
         self.bits, self.pi, self.G, self.Hq = bits, pi, group, group * kv_heads
         self.lens = np.asarray(lens, np.int32)
@@ -36,6 +36,7 @@ class Case:
         self.v = synth.normal_f16(seed, "v", (batch, kv_heads, max(total, 1), d))
         self.q = synth.normal_f16(seed, "q", (batch, self.Hq, d))
         self.rounding = rounding
+        self.qp_bits = qp_bits
         if paged_page:
             self.page_tokens = paged_page
             lens_cap = np.maximum(self.lens + spare_tokens, 1)
@@ -46,7 +47,7 @@ class Case:
             cap = max(pi, ((total + pi - 1) // pi) * pi)
             self.page_tokens = cap
             self.table_np, self.table, self.num_pages = None, None, batch
-        self.layout = hk.hack_kv_layout_make(d, kv_heads, bits, pi, self.page_tokens, 8, rounding, seed)
+        self.layout = hk.hack_kv_layout_make(d, kv_heads, bits, pi, self.page_tokens, qp_bits, rounding, seed)
         self.cache = hk.KVCache(self.layout, self.num_pages, batch, self.table, DEV)
         self.lens_dev = torch.from_numpy(self.lens.copy()).to(DEV)
 

@@ -49,8 +49,10 @@ def test_layout_make_validation(lib):
         with pytest.raises(hk.HackError) as e:
             hk.hack_kv_layout_make(*args)
         assert e.value.status == 1
-    with pytest.raises(hk.HackError):
-        hk.hack_kv_layout_make(128, 8, 2, 32, 256, qp_bits=4)
+    for qp in (0, 2, 5, 7, 16):
+        with pytest.raises(hk.HackError):
+            hk.hack_kv_layout_make(128, 8, 2, 32, 256, qp_bits=qp)
+    assert hk.hack_kv_layout_make(128, 8, 2, 32, 256, qp_bits=4).qp_bits == 4
     with pytest.raises(hk.HackError):
         hk.hack_kv_layout_make(128, 8, 2, 32, 256, rounding=7)
     assert lib.hack_kv_layout_make(None, 128, 8, 2, 32, 256, 8, 0, 0) == 1

@@ -22,13 +22,14 @@ def _gpu():
     return gpu_util
 
 
-@pytest.mark.parametrize("bits,pi,group", [(2, 32, 4), (4, 32, 8), (2, 64, 1), (4, 64, 4)])
-def test_qk_products_bit_exact(bits, pi, group):
+@pytest.mark.parametrize("bits,pi,group,qp", [(2, 32, 4, 8), (4, 32, 8, 8), (2, 64, 1, 8), (4, 64, 4, 8),
+                                              (2, 32, 4, 4), (4, 64, 8, 4)])
+def test_qk_products_bit_exact(bits, pi, group, qp):
     gu = _gpu()
     from paper_2502_03589_amd import hack as hk
     lens = [1, 47, 300]
-    gu.announce(f"qk products bits={bits} pi={pi} G={group} lens={lens}")
-    case = gu.Case(5 + bits, len(lens), 2, lens, bits, pi, group=group).quantize()
+    gu.announce(f"qk products bits={bits} pi={pi} G={group} qp={qp} lens={lens}")
+    case = gu.Case(5 + bits, len(lens), 2, lens, bits, pi, group=group, qp_bits=qp).quantize()
     qc, qm, prod = hk.hack_debug_qk_products(case.layout, case.cache, torch.from_numpy(case.q).to(gu.DEV),
                                              case.lens_dev, case.max_len)
     torch.cuda.synchronize()
@@ -37,7 +38,7 @@ def test_qk_products_bit_exact(bits, pi, group):
     for b in range(case.batch):
         for h in range(case.Hq):
             sq = seqs[b][h // group]
-            S, prods, qcodes, qmin, qscale = O.scores(case.q[b, h], sq)
+            S, prods, qcodes, qmin, qscale = O.scores(case.q[b, h], sq, qp)
             assert np.array_equal(qc[b, h], qcodes)
             assert np.array_equal(qm[b, h, :, 0].astype(np.float64), qmin)
             assert np.array_equal(qm[b, h, :, 1].astype(np.float64), qscale)
@@ -76,28 +77,31 @@ def test_pv_products_bit_exact(bits, pi, group):
 
 
 CASES = [
-    # bits, pi, group, kv_heads, lens, tail_mode, paged page
-    (2, 32, 4, 2, [256, 1, 31, 33, 300], 0, 0),
-    (2, 32, 4, 2, [256, 1, 31, 33, 300], 1, 0),
-    (4, 32, 8, 2, [77, 129, 1000], 0, 0),
-    (2, 64, 1, 3, [64, 65, 500], 0, 0),
-    (4, 64, 2, 2, [63, 700, 1], 1, 0),
-    (2, 32, 8, 1, [2048 + 17, 400], 0, 256),
-    (2, 32, 4, 2, [0, 50, 5000], 0, 128),
+    # bits, pi, group, kv_heads, lens, tail_mode, paged page, Q/P bits
+    (2, 32, 4, 2, [256, 1, 31, 33, 300], 0, 0, 8),
+    (2, 32, 4, 2, [256, 1, 31, 33, 300], 1, 0, 8),
+    (4, 32, 8, 2, [77, 129, 1000], 0, 0, 8),
+    (2, 64, 1, 3, [64, 65, 500], 0, 0, 8),
+    (4, 64, 2, 2, [63, 700, 1], 1, 0, 8),
+    (2, 32, 8, 1, [2048 + 17, 400], 0, 256, 8),
+    (2, 32, 4, 2, [0, 50, 5000], 0, 128, 8),
+    (2, 32, 4, 2, [256, 1, 31, 33, 300], 0, 0, 4),
+    (4, 64, 8, 2, [77, 129, 1000], 1, 0, 4),
 ]
 
 
-@pytest.mark.parametrize("bits,pi,group,H,lens,tail_mode,paged", CASES)
-def test_attend_decode_matches_oracle(bits, pi, group, H, lens, tail_mode, paged):
+@pytest.mark.parametrize("bits,pi,group,H,lens,tail_mode,paged,qp", CASES)
+def test_attend_decode_matches_oracle(bits, pi, group, H, lens, tail_mode, paged, qp):
     gu = _gpu()
     from paper_2502_03589_amd import hack as hk
-    gu.announce(f"decode bits={bits} pi={pi} G={group} H={H} lens={lens} tail={tail_mode} paged={paged}")
-    case = gu.Case(31 + bits + pi + group, len(lens), H, lens, bits, pi, group=group, paged_page=paged).quantize()
+    gu.announce(f"decode bits={bits} pi={pi} G={group} H={H} lens={lens} tail={tail_mode} paged={paged} qp={qp}")
+    case = gu.Case(31 + bits + pi + group, len(lens), H, lens, bits, pi, group=group, paged_page=paged,
+                   qp_bits=qp).quantize()
     out = hk.hack_attend_decode(case.layout, case.cache, torch.from_numpy(case.q).to(gu.DEV), case.lens_dev,
                                 case.max_len, tail_mode)
     torch.cuda.synchronize()
     got = out.cpu().numpy()
-    ref = O.attend_decode(case.q, case.oracle_seqs(), H, 8, tail_mode)
+    ref = O.attend_decode(case.q, case.oracle_seqs(), H, qp, tail_mode)
     err = gu.rel_err(got, ref)
     print(f"max|d|/|O|inf = {err:.3e}")
     assert err <= TOL
@@ -145,7 +149,11 @@ def test_full_size_llama8b_decode_sampled():
     got_rows = np.stack([got[b, h] for b, h in rows])
     ref_rows = np.stack([ref[b, h] for b, h in rows])
     err = float(np.abs(got_rows - ref_rows).max() / np.abs(ref_rows).max())
-    print(f"sampled rows max|d|/|O|inf = {err:.3e}")
+    # context only (not a gate): the same rows against unquantized float64 attention
+    exact = np.stack([O.attention_unquantized(case.q[b, hq], case.k[b, hq // 4], case.v[b, hq // 4])
+                      for b, hq in rows])
+    ctx = float(np.abs(got_rows - exact).max() / np.abs(exact).max())
+    print(f"sampled rows max|d|/|O|inf = {err:.3e} vs the oracle; {ctx:.3e} vs unquantized attention")
     assert err <= TOL
 
 

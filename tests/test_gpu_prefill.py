@@ -29,26 +29,28 @@ def _run_prefill(gu, case, causal):
 
 
 CASES = [
-    # bits, pi, group, kv_heads, L, causal, paged page
-    (4, 64, 4, 2, 200, True, 0),
-    (4, 64, 4, 2, 200, False, 0),
-    (2, 32, 4, 2, 131, True, 0),
-    (2, 64, 8, 1, 96, True, 0),
-    (4, 32, 1, 2, 33, True, 0),
-    (2, 32, 2, 1, 1, True, 0),
-    (4, 64, 4, 1, 64, True, 128),
-    (2, 32, 4, 1, 300, False, 64),
+    # bits, pi, group, kv_heads, L, causal, paged page, Q/P bits
+    (4, 64, 4, 2, 200, True, 0, 8),
+    (4, 64, 4, 2, 200, False, 0, 8),
+    (2, 32, 4, 2, 131, True, 0, 8),
+    (2, 64, 8, 1, 96, True, 0, 8),
+    (4, 32, 1, 2, 33, True, 0, 8),
+    (2, 32, 2, 1, 1, True, 0, 8),
+    (4, 64, 4, 1, 64, True, 128, 8),
+    (2, 32, 4, 1, 300, False, 64, 8),
+    (4, 64, 4, 2, 200, True, 0, 4),
+    (2, 32, 8, 1, 131, False, 0, 4),
 ]
 
 
-@pytest.mark.parametrize("bits,pi,group,H,L,causal,paged", CASES)
-def test_attend_prefill_matches_oracle(bits, pi, group, H, L, causal, paged):
+@pytest.mark.parametrize("bits,pi,group,H,L,causal,paged,qp", CASES)
+def test_attend_prefill_matches_oracle(bits, pi, group, H, L, causal, paged, qp):
     gu = _gpu()
-    gu.announce(f"prefill bits={bits} pi={pi} G={group} H={H} L={L} causal={causal} paged={paged}")
+    gu.announce(f"prefill bits={bits} pi={pi} G={group} H={H} L={L} causal={causal} paged={paged} qp={qp}")
     case = gu.Case(300 + bits + pi + L, 1 if L > 150 else 2, H, [L] * (1 if L > 150 else 2), bits, pi,
-                   group=group, paged_page=paged).quantize()
+                   group=group, paged_page=paged, qp_bits=qp).quantize()
     Q, got = _run_prefill(gu, case, causal)
-    ref = O.attend_prefill(Q, case.oracle_seqs(), H, causal=causal)
+    ref = O.attend_prefill(Q, case.oracle_seqs(), H, causal=causal, qp_bits=qp)
     err = gu.rel_err(got, ref)
     print(f"max|d|/|O|inf = {err:.3e}")
     assert err <= TOL
@@ -69,7 +71,11 @@ def test_prefill_full_size_sampled_rows():
     g = np.stack([got[b, h, i] for b, h, i in rows])
     r = np.stack([ref[b, h, i] for b, h, i in rows])
     err = float(np.abs(g - r).max() / np.abs(r).max())
-    print(f"sampled rows max|d|/|O|inf = {err:.3e}")
+    # context only (not a gate): the same rows against unquantized float64 attention
+    exact = np.stack([O.attention_unquantized(Q[b, h, i], case.k[b, h // 4], case.v[b, h // 4], causal_row=i)
+                      for b, h, i in rows])
+    ctx = float(np.abs(g - exact).max() / np.abs(exact).max())
+    print(f"sampled rows max|d|/|O|inf = {err:.3e} vs the oracle; {ctx:.3e} vs unquantized attention")
     assert err <= TOL
 
 
