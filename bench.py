@@ -97,7 +97,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prefill", action="store_true")
     ap.add_argument("--prefill-iters", type=int, default=10)
-    ap.add_argument("--workload", choices=["decode_70b_ragged", "decode_long_l131072", "sweep_bits_partition"],
+    ap.add_argument("--workload", choices=["decode_tiny_l256", "decode_70b_ragged", "decode_long_l131072",
+                                           "sweep_bits_partition"],
                     default=None,
                     help="time another decode workload instead (one JSON line per configuration; "
                          "not the headline line)")
@@ -376,6 +377,37 @@ def bench_workload(name: str, steps: int, warmup: int):
                               "bytes_per_call": int(nbytes), "bytes_per_token_head": round(nbytes / (B * H * L), 2),
                               "frac_of_8TBs": round(nbytes / ms / 1e6 / HBM_PEAK_GBS, 4)}), flush=True)
             del caches, calls
+        return
+    if name == "decode_tiny_l256":
+        # one decode call of batch 1, one q / kv head, 256 tokens: launch-latency sized, so
+        # the figure is microseconds per call; 64 replicas keep the inputs out of the caches
+        L, R = wl.context, 64
+        lay = hk.hack_kv_layout_make(d, H, wl.kv_bits, pi, L)
+        k = torch.from_numpy(synth.normal_f16(wl.seed, "k", (B, H, L, d))).to(dev)
+        v = torch.from_numpy(synth.normal_f16(wl.seed, "v", (B, H, L, d))).to(dev)
+        q = torch.from_numpy(synth.normal_f16(wl.seed, "q", (B, Hq, d))).to(dev)
+        ln = torch.full((B,), L, dtype=torch.int32, device=dev)
+        caches = [hk.KVCache(lay, B, B, None, dev) for _ in range(R)]
+        for cache in caches:
+            hk.hack_quantize(lay, cache, k, v, ln, L)
+        ws = hk.decode_workspace(lay, B, Hq, L)
+        out = torch.empty((B, Hq, d), dtype=torch.float32, device=dev)
+        calls = [hk.bind_attend_decode(lay, cache, q, ln, L, hk.TAIL_FP16, out, ws) for cache in caches]
+        for i in range(warmup):
+            calls[i % R]()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for i in range(steps):
+            calls[i % R]()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        nbytes = B * H * decode_bytes_per_seq_head(L, d, wl.kv_bits, pi, lay.sum_bytes) + B * Hq * d * 6
+        print(json.dumps({"workload": name, "metric": "decode us per call", "value": round(ms * 1e3, 2),
+                          "unit": "us", "GBs": round(nbytes / ms / 1e6, 2), "bytes_per_call": int(nbytes),
+                          "note": "back-to-back calls; launch-latency bound, % of HBM peak not meaningful"}),
+              flush=True)
         return
     if name == "decode_70b_ragged":
         lens = synth.uniform_lengths(wl.seed, B, *wl.len_range)

@@ -42,6 +42,7 @@ struct DecodeArgs {
   int32_t* counters;      // [B][H_kv] chunks finished (zero between calls)
   int num_q_heads;
   int group;              // H_q / H_kv
+  int head_groups;        // workgroups per (sequence, kv head, chunk), each for up to 4*GT heads
   int chunk;
   int splits;
   int tail_requant;

@@ -264,13 +264,13 @@ __device__ __forceinline__ float ld_rec(const float* p) {
 }
 
 template <bool COHERENT>
-__device__ __forceinline__ void merge_chunks(const DecodeArgs& a, int s, int hkv, int Lraw) {
+__device__ __forceinline__ void merge_chunks(const DecodeArgs& a, int s, int hkv, int Lraw, int head0, int Gl) {
   constexpr int D = 128, REC = 4 + D, U = 8;
   const int G = a.group, Hq = a.num_q_heads;
   const int64_t pair = (int64_t)s * a.c.kv_heads + hkv;
   // thread (head gh, channels 4*q .. 4*q+3)
-  for (int idx = threadIdx.x; idx < G * (D / 4); idx += blockDim.x) {
-    const int gh = idx / (D / 4), ch = 4 * (idx % (D / 4));
+  for (int idx = threadIdx.x; idx < Gl * (D / 4); idx += blockDim.x) {
+    const int gh = head0 + idx / (D / 4), ch = 4 * (idx % (D / 4));
     float mrun = -INFINITY, lsum = 0.0f;
     float4 o = {0.0f, 0.0f, 0.0f, 0.0f};
     for (int sp0 = 0; sp0 < a.splits; sp0 += U) {
@@ -323,9 +323,14 @@ __device__ __forceinline__ void merge_chunks(const DecodeArgs& a, int s, int hkv
   }
 }
 
-template <int BITS, int PI, int GT, int MODE>
+template <int BITS, int PI, int GT, int MODE, int QP>
 __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decode_kernel(DecodeArgs a) {
   constexpr int D = 128;
+  // Q and P codes of QP bits: 2^QP - 1 levels; they enter the signed MFMA as code - 2^(QP-1)
+  constexpr float kQmax = (float)((1 << QP) - 1);
+  constexpr float kInvQmax = 1.0f / kQmax;
+  constexpr int kQoff = 1 << (QP - 1);
+  constexpr float kQoffF = (float)kQoff;
   constexpr int P = D / PI;          // K partitions per token
   constexpr int QPP = 4 / P;         // channel quarters per partition
   constexpr int TILES = PI / 16;     // 16-token tiles per V block
@@ -354,8 +359,13 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
   // chunk index slowest: every (sequence, head) pair's first chunks are dispatched
   // before any pair's later ones, so a long sequence's chunks do not queue behind
   // the short sequences of a ragged batch
-  const int s = blockIdx.y, hkv = blockIdx.x, split = blockIdx.z;
   const int G = a.group, Hq = a.num_q_heads, H = c.kv_heads;
+  // a kv group of more than HT heads is split over workgroups (blockIdx.x = hg * H + hkv,
+  // so the workgroups of one chunk are H apart in the grid and share an XCD's L2)
+  const bool one_group = a.head_groups == 1;
+  const int s = blockIdx.y, split = blockIdx.z;
+  const int hkv = one_group ? (int)blockIdx.x : (int)blockIdx.x % H, hg = one_group ? 0 : (int)blockIdx.x / H;
+  const int head0 = HT * hg, Gl = min(HT, G - head0);  // this workgroup's heads of the group
   // lengths outside [0, max_len] break the caller contract; clamp so that every
   // access stays inside the cache and the workspace
   // this wave's query values (head slots wave, wave + 4, ...) do not depend on the
@@ -364,8 +374,8 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
 #pragma unroll
   for (int i = 0; i < GT; ++i) {
     const int gh = wave + kWaves * i;
-    qraw[i] = (MODE != MODE_PV && gh < G)
-                  ? reinterpret_cast<const uint32_t*>(a.q + ((int64_t)s * Hq + hkv * G + gh) * D)[lane]
+    qraw[i] = (MODE != MODE_PV && gh < Gl)
+                  ? reinterpret_cast<const uint32_t*>(a.q + ((int64_t)s * Hq + hkv * G + head0 + gh) * D)[lane]
                   : 0u;
   }
   const int Lin = a.lens[s];
@@ -377,7 +387,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
     // the new length goes to a separate array so no workgroup sees it half-way.
     const bool ok = Lin >= 0 && Lin < a.capacity && Lin + 1 <= a.max_len;
     Lq = ok ? Lin + 1 : Lq;
-    if (split == 0 && hkv == 0 && tid == 0) a.lens_out[s] = Lq;
+    if (split == 0 && blockIdx.x == 0 && tid == 0) a.lens_out[s] = Lq;
     if (ok && Lin / a.chunk == split) {
       append_head<BITS, PI>(c, a.k_new + ((int64_t)s * H + hkv) * D, a.v_new + ((int64_t)s * H + hkv) * D, s, hkv,
                             Lin, a.tail_requant != 0, a.stochastic != 0, a.key_k, a.key_v, tid, 256);
@@ -388,7 +398,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
   const int L = Lq;
   if (t0 >= L) {
     if (MODE == MODE_ATTEND && split == 0) {  // empty sequence: zeros
-      for (int i = tid; i < G * D; i += 256) a.out[((int64_t)s * Hq + hkv * G) * D + i] = 0.0f;
+      for (int i = tid; i < Gl * D; i += 256) a.out[((int64_t)s * Hq + hkv * G + head0) * D + i] = 0.0f;
     }
     return;
   }
@@ -404,8 +414,8 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
 #pragma unroll
     for (int i = 0; i < GT; ++i) {
       const int gh = wave + kWaves * i;
-      const bool real = gh < G;
-      const int hq = hkv * G + gh;
+      const bool real = gh < Gl;
+      const int hq = hkv * G + head0 + gh;
       float x0 = 0.0f, x1 = 0.0f;
       if (real) {
         const float2 f = __half22float2(*reinterpret_cast<const __half2*>(&qraw[i]));
@@ -421,11 +431,11 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
       float sq, c0 = 0.0f, c1 = 0.0f;
       {
 #pragma clang fp contract(off)
-        sq = __fdiv_rn(__fsub_rn(mx, mn), a.qmax);
+        sq = __fdiv_rn(__fsub_rn(mx, mn), kQmax);
         if (sq != 0.0f) {
           const float r = __fdiv_rn(1.0f, sq);
-          c0 = fminf(rintf(__fmul_rn(__fsub_rn(x0, mn), r)), a.qmax);
-          c1 = fminf(rintf(__fmul_rn(__fsub_rn(x1, mn), r)), a.qmax);
+          c0 = fminf(rintf(__fmul_rn(__fsub_rn(x0, mn), r)), kQmax);
+          c1 = fminf(rintf(__fmul_rn(__fsub_rn(x1, mn), r)), kQmax);
         }
       }
       int csum = (int)c0 + (int)c1;
@@ -434,14 +444,14 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
       {
         const int ch = 2 * lane;  // channels ch, ch + 1 share quarter and slice
         const int g = ch >> 5, m = (ch >> 4) & 1, e = ch & 15;
-        q_lds[gh][g][m][perm_position<BITS>(e)] = real ? (int8_t)((int)c0 - a.qoff) : (int8_t)0;
-        q_lds[gh][g][m][perm_position<BITS>(e + 1)] = real ? (int8_t)((int)c1 - a.qoff) : (int8_t)0;
+        q_lds[gh][g][m][perm_position<BITS>(e)] = real ? (int8_t)((int)c0 - kQoff) : (int8_t)0;
+        q_lds[gh][g][m][perm_position<BITS>(e + 1)] = real ? (int8_t)((int)c1 - kQoff) : (int8_t)0;
       }
       const int p = (2 * lane) / PI;
       if ((2 * lane) % PI == 0) {
         // per partition: s_q, m~_q = m_q + qoff s_q, R = s_q sum q' + n m_q (all in log2 units)
         qm_lds[gh][p][0] = real ? kScoreScale * sq : 0.0f;
-        qm_lds[gh][p][1] = real ? kScoreScale * (mn + a.qoff_f * sq) : 0.0f;
+        qm_lds[gh][p][1] = real ? kScoreScale * (mn + kQoffF * sq) : 0.0f;
         qm_lds[gh][p][2] = real ? kScoreScale * (sq * (float)csum + (float)PI * mn) : 0.0f;
         if (MODE == MODE_QK && real && split == 0) {
           a.dbg_qmeta[(((int64_t)s * Hq + hq) * P + p) * 2 + 0] = mn;
@@ -592,20 +602,20 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
           const int rt = i / (4 * PI), hh = (i / PI) & 3, e = i % PI;
           const int gh = rt * 4 + hh;
           int8_t v = 0;
-          if (present && kb < F && gh < G)
-            v = (int8_t)((int)a.dbg_pcodes[(((int64_t)s * Hq + hkv * G + gh) * NB + kb) * PI + e] - a.qoff);
+          if (present && kb < F && gh < Gl)
+            v = (int8_t)((int)a.dbg_pcodes[(((int64_t)s * Hq + hkv * G + head0 + gh) * NB + kb) * PI + e] - kQoff);
           wl.p[rt][k][hh][(e >> 4) * 16 + perm_position<BITS>(e & 15)] = v;
         }
         if (lane < HT) {
           const int rt = lane >> 2, hh = lane & 3, gh = lane;
           float pm = 0.0f, ps = 0.0f;
-          if (present && kb < F && gh < G) {
-            const int64_t base = ((int64_t)s * Hq + hkv * G + gh) * NB + kb;
+          if (present && kb < F && gh < Gl) {
+            const int64_t base = ((int64_t)s * Hq + hkv * G + head0 + gh) * NB + kb;
             pm = a.dbg_pmeta[base * 2 + 0];
             ps = a.dbg_pmeta[base * 2 + 1];
           }
           wl.pst[rt][k][0][hh] = ps;
-          wl.pst[rt][k][1][hh] = pm + a.qoff_f * ps;
+          wl.pst[rt][k][1][hh] = pm + kQoffF * ps;
         }
         continue;
       } else {
@@ -642,13 +652,13 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
               int zq[P];
 #pragma unroll
               for (int p = 0; p < P; ++p) zq[p] = __shfl((int)d.kz[ti], 16 * (p * QPP) + col, 64);
-              if (tok < L && gh < G) {
+              if (tok < L && gh < Gl) {
 #pragma unroll
                 for (int p = 0; p < P; ++p) {
-                  int v = a.qoff * zq[p];
+                  int v = kQoff * zq[p];
 #pragma unroll
                   for (int q = p * QPP; q < (p + 1) * QPP; ++q) v += acc[q];
-                  a.dbg_prod[(((int64_t)s * Hq + hkv * G + gh) * a.max_len + tok) * P + p] = v;
+                  a.dbg_prod[(((int64_t)s * Hq + hkv * G + head0 + gh) * a.max_len + tok) * P + p] = v;
                 }
               }
             }
@@ -685,16 +695,16 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
             const float pmax = __builtin_amdgcn_exp2f(bmax - mr);
             const float pmin = __builtin_amdgcn_exp2f(bmin - mr);
             const float dp = pmax - pmin;
-            const float r = dp > 0.0f ? a.qmax * __builtin_amdgcn_rcpf(dp) : 0.0f;
+            const float r = dp > 0.0f ? kQmax * __builtin_amdgcn_rcpf(dp) : 0.0f;
             const float bias = -pmin * r;
 #pragma unroll
             for (int tl = 0; tl < TILES; ++tl) {
               // round-to-nearest-even with saturation (codes stay within [0, qmax])
               const uint32_t code = __builtin_amdgcn_cvt_pk_u8_f32(fmaf(pt[tl], r, bias), 0, 0u);
               const bool valid = full || bt0 + 16 * tl + col < L;
-              wl.p[rt][k][grp][tl * 16 + perm_position<BITS>(col)] = valid ? (int8_t)((int)code - a.qoff) : (int8_t)0;
+              wl.p[rt][k][grp][tl * 16 + perm_position<BITS>(col)] = valid ? (int8_t)((int)code - kQoff) : (int8_t)0;
             }
-            ps_s[rt][k] = dp * a.inv_qmax;
+            ps_s[rt][k] = dp * kInvQmax;
             ps_m[rt][k] = pmin;
           } else {
 #pragma unroll
@@ -716,7 +726,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
           for (int k = 0; k < 4; ++k) {
             const float f = __builtin_amdgcn_exp2f(m_blk[rt][k] - m_ref[rt]);
             wl.pst[rt][k][0][grp] = ps_s[rt][k] * f;
-            wl.pst[rt][k][1][grp] = (ps_m[rt][k] + a.qoff_f * ps_s[rt][k]) * f;
+            wl.pst[rt][k][1][grp] = (ps_m[rt][k] + kQoffF * ps_s[rt][k]) * f;
             if (k == kF) wl.tailf[rt][grp] = f;
           }
           wl.alpha[rt][grp] = __builtin_amdgcn_exp2f(m_start[rt] - m_ref[rt]);
@@ -819,9 +829,9 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               const int gh = rt * 4 + i;
-              if (gvalid && gh < G)
-                a.dbg_prod[(((int64_t)s * Hq + hkv * G + gh) * (a.max_len / PI) + vkb) * D + 8 * col + j] =
-                    acc[i] + a.qoff * (int)zj;
+              if (gvalid && gh < Gl)
+                a.dbg_prod[(((int64_t)s * Hq + hkv * G + head0 + gh) * (a.max_len / PI) + vkb) * D + 8 * col + j] =
+                    acc[i] + kQoff * (int)zj;
             }
           }
         }
@@ -870,6 +880,12 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
   }
   if constexpr (MODE == MODE_QK) return;
 
+  // this workgroup's heads, recomputed from the grid index instead of being kept live
+  // across the span loop (where they would take scalar registers)
+  int bx = (int)blockIdx.x;
+  asm volatile("" : "+s"(bx));
+  const int hg_e = a.head_groups == 1 ? 0 : bx / H, head0_e = HT * hg_e, Gl_e = min(HT, G - head0_e);
+
   // ---- wave result: O summed over the 4 lane groups (block slots), max and sum per head ----
 #pragma unroll
   for (int rt = 0; rt < GT; ++rt) {
@@ -891,7 +907,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
   // ---- merge the four waves: thread (head slot, channel pair) ----
   const int64_t pair = (int64_t)s * H + hkv;
   constexpr int REC = 4 + D;  // max, sum, 2 pad, O
-  for (int idx = tid; idx < G * (D / 2); idx += 256) {
+  for (int idx = tid; idx < Gl_e * (D / 2); idx += 256) {
     const int gh = idx / (D / 2), ch = 2 * (idx % (D / 2));
     float mmax = -INFINITY;
 #pragma unroll
@@ -907,7 +923,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
         o1 = fmaf(wl_all[w].mrg_o[gh][ch + 1], wt, o1);
       }
     }
-    float* o = a.out + ((int64_t)s * Hq + hkv * G + gh) * D + ch;
+    float* o = a.out + ((int64_t)s * Hq + hkv * G + head0_e + gh) * D + ch;
     if (MODE == MODE_PV) {
       o[0] = o0;
       o[1] = o1;
@@ -916,7 +932,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
       o[0] = o0 * inv;
       o[1] = o1 * inv;
     } else {
-      float* rec = a.partials + ((pair * a.splits + split) * G + gh) * REC;
+      float* rec = a.partials + ((pair * a.splits + split) * G + head0_e + gh) * REC;
       if constexpr (HACK_DECODE_FUSED_MERGE == 2) {
         // agent-coherent (write-through) stores: complete at the device's coherence
         // point once the wave's store counter drains
@@ -944,18 +960,18 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
     __syncthreads();
     if (tid == 0) {
 #if HACK_DECODE_FUSED_MERGE == 2
-      const int done = __hip_atomic_fetch_add(&a.counters[pair], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const int done = __hip_atomic_fetch_add(&a.counters[pair * a.head_groups + hg_e], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 #else
       // acquire-release: publishes this chunk's record, and for the last arriver
       // makes every other chunk's record visible
-      const int done = __hip_atomic_fetch_add(&a.counters[pair], 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+      const int done = __hip_atomic_fetch_add(&a.counters[pair * a.head_groups + hg_e], 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
 #endif
       last_chunk = done == nsplit - 1;
     }
     __syncthreads();
     if (last_chunk) {
-      merge_chunks<HACK_DECODE_FUSED_MERGE == 2>(a, s, hkv, L);
-      if (tid == 0) __hip_atomic_store(&a.counters[pair], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      merge_chunks<HACK_DECODE_FUSED_MERGE == 2>(a, s, hkv, L, head0_e, Gl_e);
+      if (tid == 0) __hip_atomic_store(&a.counters[pair * a.head_groups + hg_e], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
 #endif
@@ -967,7 +983,7 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeArgs a) {
   const int Lraw = a.k_new != nullptr ? a.lens[s] + 1 : a.lens[s];  // a decode step attends lens + 1
   const int L = max(0, min(Lraw, a.max_len));
   if ((L + a.chunk - 1) / a.chunk <= 1) return;  // written directly by the attention kernel
-  merge_chunks<false>(a, s, hkv, Lraw);
+  merge_chunks<false>(a, s, hkv, Lraw, 0, a.group);
 }
 
 constexpr int64_t kMaxWgSpans = 64;
@@ -976,8 +992,16 @@ constexpr int64_t kMaxGridZ = 65535;
 // Workgroups per compute unit the grid is sized for.  The 2-bit, partition-32 kernel
 // with one row tile uses about 145 VGPRs, so three waves per SIMD are resident even
 // though it is compiled for two (measured best on the 4K-context decode workload).
+#ifndef HACK_DECODE_HEAD_SPLIT
+#define HACK_DECODE_HEAD_SPLIT 1  // groups of more than 4 heads: one-tile workgroups per 4 heads
+#endif
+
+// Row tiles (of 4 heads) per workgroup, and workgroups per (sequence, kv head, chunk).
+static int row_tiles_of(int G) { return (G <= 4 || HACK_DECODE_HEAD_SPLIT) ? 1 : 2; }
+static int head_groups_of(int G) { return (G + 4 * row_tiles_of(G) - 1) / (4 * row_tiles_of(G)); }
+
 static int occupancy_of(const hack_kv_layout& lay, int G) {
-  const int gt = G <= 4 ? 1 : 2;
+  const int gt = row_tiles_of(G);
   if (lay.kv_bits == 2 && lay.partition == 32 && gt == 1) return decode_occupancy<2, 32, 1>() + 1;
   return 2;
 }
@@ -987,11 +1011,12 @@ DecodePlan plan_decode(const hack_kv_layout& lay, int batch, int num_q_heads, in
   const int64_t span = 4 * lay.partition;
   const int64_t pairs = (int64_t)batch * lay.num_kv_heads;
   const int64_t G = lay.num_kv_heads > 0 ? num_q_heads / lay.num_kv_heads : 0;
+  const int64_t nhg = G > 0 ? head_groups_of((int)G) : 1;
   // one workgroup per compute unit and resident wave slot of a SIMD
   const int64_t per_cu = HACK_DECODE_WGS_PER_CU > 0 ? HACK_DECODE_WGS_PER_CU : occupancy_of(lay, (int)G);
   const int64_t target = kComputeUnits * per_cu;
   const int64_t spans_seq = ((int64_t)max_len + span - 1) / span;
-  int64_t wg_spans = pairs > 0 ? (spans_seq * pairs + target - 1) / target : 1;
+  int64_t wg_spans = pairs > 0 ? (spans_seq * pairs * nhg + target - 1) / target : 1;
   if (wg_spans < 1) wg_spans = 1;
   // A chunk of at most kMaxWgSpans spans bounds the time one workgroup holds a slot:
   // in a ragged batch the longest sequence then spreads over more workgroups than an
@@ -1005,34 +1030,47 @@ DecodePlan plan_decode(const hack_kv_layout& lay, int batch, int num_q_heads, in
   p.splits = max_len > 0 ? (int)(((int64_t)max_len + p.chunk - 1) / p.chunk) : 1;
   p.partial_floats = pairs * p.splits * G * (4 + lay.head_dim);
   p.counter_offset = ((p.partial_floats * 4 + 255) / 256) * 256;
-  p.workspace_bytes = p.counter_offset + ((pairs * 4 + 255) / 256) * 256;
+  p.workspace_bytes = p.counter_offset + ((pairs * nhg * 4 + 255) / 256) * 256;
   return p;
 }
 
-template <int BITS, int PI, int GT, int MODE>
+template <int BITS, int PI, int GT, int MODE, int QP>
 static hipError_t decode_impl(const DecodeArgs& a, int batch, hipStream_t stream) {
-  dim3 grid((unsigned)a.c.kv_heads, (unsigned)batch, (unsigned)a.splits);
-  hipLaunchKernelGGL((decode_kernel<BITS, PI, GT, MODE>), grid, dim3(256), 0, stream, a);
+  dim3 grid((unsigned)(a.c.kv_heads * a.head_groups), (unsigned)batch, (unsigned)a.splits);
+  hipLaunchKernelGGL((decode_kernel<BITS, PI, GT, MODE, QP>), grid, dim3(256), 0, stream, a);
   if (MODE == MODE_ATTEND && a.splits > 1 && !HACK_DECODE_FUSED_MERGE)
     hipLaunchKernelGGL(decode_merge_kernel, dim3((unsigned)a.c.kv_heads, (unsigned)batch), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 
-template <int BITS, int PI, int GT>
+template <int BITS, int PI, int GT, int QP>
 static hipError_t decode_mode(const DecodeArgs& a, int batch, int mode, hipStream_t stream) {
   switch (mode) {
-    case MODE_ATTEND: return decode_impl<BITS, PI, GT, MODE_ATTEND>(a, batch, stream);
-    case MODE_QK: return decode_impl<BITS, PI, GT, MODE_QK>(a, batch, stream);
-    case MODE_PV: return decode_impl<BITS, PI, GT, MODE_PV>(a, batch, stream);
+    case MODE_ATTEND: return decode_impl<BITS, PI, GT, MODE_ATTEND, QP>(a, batch, stream);
+    case MODE_QK: return decode_impl<BITS, PI, GT, MODE_QK, QP>(a, batch, stream);
+    case MODE_PV: return decode_impl<BITS, PI, GT, MODE_PV, QP>(a, batch, stream);
     default: return hipErrorInvalidValue;
   }
 }
 
-template <int BITS, int PI>
-static hipError_t decode_gt(const DecodeArgs& a, int batch, int mode, hipStream_t stream) {
-  if (a.group <= 4) return decode_mode<BITS, PI, 1>(a, batch, mode, stream);
-  if (a.group <= 8) return decode_mode<BITS, PI, 2>(a, batch, mode, stream);
+template <int BITS, int PI, int GT>
+static hipError_t decode_qp(const DecodeArgs& a, int batch, int mode, hipStream_t stream) {
+  if (a.qoff == 128) return decode_mode<BITS, PI, GT, 8>(a, batch, mode, stream);
+  if (a.qoff == 8) return decode_mode<BITS, PI, GT, 4>(a, batch, mode, stream);
   return hipErrorInvalidValue;
+}
+
+template <int BITS, int PI>
+static hipError_t decode_gt(const DecodeArgs& args, int batch, int mode, hipStream_t stream) {
+  if (args.group < 1 || args.group > 8) return hipErrorInvalidValue;
+  DecodeArgs a = args;
+  a.head_groups = head_groups_of(a.group);
+  if constexpr (HACK_DECODE_HEAD_SPLIT) {
+    return decode_qp<BITS, PI, 1>(a, batch, mode, stream);
+  } else {
+    if (row_tiles_of(a.group) == 1) return decode_qp<BITS, PI, 1>(a, batch, mode, stream);
+    return decode_qp<BITS, PI, 2>(a, batch, mode, stream);
+  }
 }
 
 hipError_t launch_decode(const hack_kv_layout& lay, const DecodeArgs& a, int batch, int mode,

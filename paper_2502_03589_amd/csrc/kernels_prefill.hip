@@ -53,14 +53,21 @@ constexpr float kSlack = 8.0f;   // reference max raised only beyond this (log2 
 #define HACK_PREFILL_PV_RANK_PAIRED 1  // ... as one outer-product MFMA per two blocks (else VALU)
 #endif
 
+#ifndef HACK_PREFILL_KPAD
+#define HACK_PREFILL_KPAD 32
+#endif
+#ifndef HACK_PREFILL_VPAD
+#define HACK_PREFILL_VPAD 32
+#endif
+
 template <int PI>
 struct PrefillCfg {
   static constexpr int D = 128;
   static constexpr int P = D / PI;    // K partitions per token
   static constexpr int TL = PI / 16;  // 16-token tiles per block
   static constexpr int KSL = PI / 4;  // operand bytes per lane per MFMA (k-slots of a lane group)
-  static constexpr int KROW = D + 16; // LDS row stride of unpacked K (bytes)
-  static constexpr int VROW = PI + 16;// LDS row stride of unpacked V (bytes)
+  static constexpr int KROW = D + HACK_PREFILL_KPAD;  // LDS row stride of unpacked K (bytes)
+  static constexpr int VROW = PI + HACK_PREFILL_VPAD; // LDS row stride of unpacked V (bytes)
 };
 
 // int8 MFMA with K = PI: 16x16x64 (16 bytes per lane) or 16x16x32 (8 bytes per lane).
@@ -306,7 +313,6 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
 
   __shared__ __attribute__((aligned(16))) Stage<PI> stages[2];
   __shared__ __attribute__((aligned(16))) VMeta vm_ring[3];
-  __shared__ float ptail[8][16][PI];
 
   const CacheView& c = a.c;
   const int tid = threadIdx.x;
@@ -584,27 +590,30 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
 #if HACK_PREFILL_PV_RANK_PAIRED
       if (rk_blk >= 0) rank_pair(vmc, 0.0f, 0.0f, false);
 #endif
-      // fp16 open block: O[row][ch] += sum_{t < T} p[row][t] v_t[ch] with unquantized p
+      // fp16 open block: O[row][ch] += sum_{t < T} p[row][t] v_t[ch] with unquantized p;
+      // p[row][t] lives in lane (row, group (t mod 16) / 4) and is read by a lane shuffle
+      const __half* vt = c.v_tail + (((int64_t)s * c.kv_heads + hkv) * PI) * D;
 #pragma unroll
       for (int tl = 0; tl < TL; ++tl)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) ptail[wave][col][16 * tl + 4 * grp + i] = pt[tl][i];
-      __builtin_amdgcn_s_waitcnt(0xC07F);
-      __builtin_amdgcn_wave_barrier();
-      const __half* vt = c.v_tail + (((int64_t)s * c.kv_heads + hkv) * PI) * D;
-      for (int t = 0; t < T; ++t) {
-        const float pr = ptail[wave][col][t];
+        for (int g = 0; g < 4; ++g)
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const uint2 raw = *reinterpret_cast<const uint2*>(vt + (int64_t)t * D + 16 * j + 4 * grp);
-          const float2 v01 = __half22float2(*reinterpret_cast<const __half2*>(&raw.x));
-          const float2 v23 = __half22float2(*reinterpret_cast<const __half2*>(&raw.y));
-          o[j][0] = fmaf(pr, v01.x, o[j][0]);
-          o[j][1] = fmaf(pr, v01.y, o[j][1]);
-          o[j][2] = fmaf(pr, v23.x, o[j][2]);
-          o[j][3] = fmaf(pr, v23.y, o[j][3]);
-        }
-      }
+          for (int i = 0; i < 4; ++i) {
+            const int t = 16 * tl + 4 * g + i;
+            const float pr = __shfl(pt[tl][i], col + 16 * g, 64);
+            if (t < T) {
+#pragma unroll
+              for (int j = 0; j < 8; ++j) {
+                const uint2 raw = *reinterpret_cast<const uint2*>(vt + (int64_t)t * D + 16 * j + 4 * grp);
+                const float2 v01 = __half22float2(*reinterpret_cast<const __half2*>(&raw.x));
+                const float2 v23 = __half22float2(*reinterpret_cast<const __half2*>(&raw.y));
+                o[j][0] = fmaf(pr, v01.x, o[j][0]);
+                o[j][1] = fmaf(pr, v01.y, o[j][1]);
+                o[j][2] = fmaf(pr, v23.x, o[j][2]);
+                o[j][3] = fmaf(pr, v23.y, o[j][3]);
+              }
+            }
+          }
     }
     if (next) stage_store<BITS, PI>(sr, stages[(kb + 1) & 1], vm_ring[(kb + 1) % 3], kb + 1 < F);
     __syncthreads();  // stage kb+1 complete; stage kb free for kb+2
