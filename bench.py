@@ -353,8 +353,10 @@ def bench_workload(name: str, steps: int, warmup: int):
         q = torch.from_numpy(synth.normal_f16(base.seed, "q", (B, Hq, d))).to(dev)
         ln = torch.full((B,), L, dtype=torch.int32, device=dev)
         R = 10
-        for bits, part in ((2, 32), (2, 64), (4, 32), (4, 64)):
-            lay = hk.hack_kv_layout_make(d, H, bits, part, L)
+        for bits, part, se in ((2, 32, True), (2, 64, True), (4, 32, True), (4, 64, True),
+                               (2, 32, False), (2, 64, False), (4, 32, False), (4, 64, False)):
+            # se=False: summation elimination off, no cached sums (fewer bytes, sums rebuilt)
+            lay = hk.hack_kv_layout_make(d, H, bits, part, L, sums_cached=se)
             caches = [hk.KVCache(lay, B, B, None, dev) for _ in range(R)]
             for cache in caches:
                 hk.hack_quantize(lay, cache, k, v, ln, L)
@@ -372,7 +374,8 @@ def bench_workload(name: str, steps: int, warmup: int):
             torch.cuda.synchronize()
             ms = e0.elapsed_time(e1) / steps
             nbytes = B * H * decode_bytes_per_seq_head(L, d, bits, part, lay.sum_bytes) + B * Hq * d * 6
-            print(json.dumps({"workload": name, "kv_bits": bits, "partition": part, "metric": "decode GB/s",
+            print(json.dumps({"workload": name, "kv_bits": bits, "partition": part, "sums_cached": se,
+                              "metric": "decode GB/s",
                               "value": round(nbytes / ms / 1e6, 2), "unit": "GB/s", "us_per_call": round(ms * 1e3, 2),
                               "bytes_per_call": int(nbytes), "bytes_per_token_head": round(nbytes / (B * H * L), 2),
                               "frac_of_8TBs": round(nbytes / ms / 1e6 / HBM_PEAK_GBS, 4)}), flush=True)

@@ -88,7 +88,8 @@ typedef struct hack_kv_layout {
   int32_t qp_bits;       /* bits of the transient Q and P codes: 8 (Sec. 5.1, the
                             paper's INT8) or 4                                      */
   int32_t rounding;      /* HACK_ROUND_*                                           */
-  int32_t sum_bytes;     /* 1 if b + ceil(log2 Pi) <= 8 else 2 (Sec. 5.3, Sec. 6)  */
+  int32_t sum_bytes;     /* 1 if b + ceil(log2 Pi) <= 8 else 2 (Sec. 5.3, Sec. 6);
+                            0 when no sums are cached (hack_kv_layout_set_sums)     */
   uint64_t seed;         /* stochastic-rounding seed                               */
 } hack_kv_layout;
 
@@ -117,6 +118,16 @@ typedef struct hack_kv_cache {
 hack_status hack_kv_layout_make(hack_kv_layout* out, int32_t head_dim, int32_t num_kv_heads,
                                 int32_t kv_bits, int32_t partition, int32_t page_tokens,
                                 int32_t qp_bits, int32_t rounding, uint64_t seed);
+
+/* Summation elimination (Sec. 5.3) on or off for `layout`.  cached = 1 (the
+ * default of hack_kv_layout_make): the code sum of every partition is stored with
+ * it (K_SUMS, V_SUMS) and read by the kernels.  cached = 0: no sums are stored
+ * (their sections have 0 bytes and their pointers may be NULL); decode attention
+ * rebuilds each sum from the packed codes it has loaded.  With cached = 0,
+ * hack_attend_prefill and the debug exports return HACK_ERR_UNSUPPORTED.  Returns
+ * HACK_ERR_INVALID_ARGUMENT for a null or invalid layout or cached not in {0,1}.
+ * Host only. */
+hack_status hack_kv_layout_set_sums(hack_kv_layout* layout, int32_t cached);
 
 /* Bytes of one cache section: `count` is the number of pages for the K_* and V_*
  * code/meta/sum sections and the number of sequences for V_TAIL.  Returns -1 for a

@@ -10,6 +10,13 @@ namespace {
 
 constexpr int kMaxGridYZ = 65535;  // largest y or z extent of a launch grid
 
+// Bytes of one cached code sum: b + ceil(log2 pi) bits rounded up to 1 or 2 bytes.
+int sum_width(int bits, int pi) {
+  int need = bits;
+  for (int v = 1; v < pi && v > 0; v <<= 1) ++need;
+  return need <= 8 ? 1 : 2;
+}
+
 bool layout_ok(const hack_kv_layout* l) {
   if (!l) return false;
   const int pi = l->partition;
@@ -20,16 +27,14 @@ bool layout_ok(const hack_kv_layout* l) {
   if (l->page_tokens <= 0 || l->page_tokens % pi != 0) return false;
   if (!(l->qp_bits == 8 || l->qp_bits == 4)) return false;
   if (!(l->rounding == HACK_ROUND_NEAREST_EVEN || l->rounding == HACK_ROUND_STOCHASTIC)) return false;
-  int need = l->kv_bits;
-  for (int v = 1; v < pi; v <<= 1) ++need;  // b + ceil(log2 pi)
-  return l->sum_bytes == (need <= 8 ? 1 : 2);
+  return l->sum_bytes == 0 || l->sum_bytes == sum_width(l->kv_bits, pi);
 }
 
 // Validates the cache pointers for `batch` sequences; returns the per-sequence capacity or -1.
 int64_t cache_capacity(const hack_kv_layout* l, const hack_kv_cache* c, int batch) {
   if (!c) return -1;
-  if (!c->k_codes || !c->k_meta || !c->k_sums || !c->v_codes || !c->v_meta || !c->v_sums || !c->v_tail)
-    return -1;
+  if (!c->k_codes || !c->k_meta || !c->v_codes || !c->v_meta || !c->v_tail) return -1;
+  if (l->sum_bytes != 0 && (!c->k_sums || !c->v_sums)) return -1;
   if (c->num_pages <= 0) return -1;
   if (c->block_table_dev) {
     if (c->max_blocks_per_seq <= 0) return -1;
@@ -87,11 +92,15 @@ hack_status hack_kv_layout_make(hack_kv_layout* out, int32_t head_dim, int32_t n
   l.qp_bits = qp_bits;
   l.rounding = rounding;
   l.seed = seed;
-  int need = kv_bits;
-  for (int v = 1; v < partition && v > 0; v <<= 1) ++need;
-  l.sum_bytes = need <= 8 ? 1 : 2;
+  l.sum_bytes = sum_width(kv_bits, partition);
   if (!layout_ok(&l)) return HACK_ERR_INVALID_ARGUMENT;
   *out = l;
+  return HACK_OK;
+}
+
+hack_status hack_kv_layout_set_sums(hack_kv_layout* layout, int32_t cached) {
+  if (!layout_ok(layout) || !(cached == 0 || cached == 1)) return HACK_ERR_INVALID_ARGUMENT;
+  layout->sum_bytes = cached ? sum_width(layout->kv_bits, layout->partition) : 0;
   return HACK_OK;
 }
 
@@ -241,6 +250,7 @@ hack_status hack_attend_prefill(const hack_kv_layout* layout, const hack_kv_cach
   if (!layout_ok(layout) || !q_dev || !out_dev || batch < 0 || len < 0) return HACK_ERR_INVALID_ARGUMENT;
   const hack_status sh = attention_shape(layout, num_q_heads);
   if (sh != HACK_OK) return sh;
+  if (layout->sum_bytes == 0) return HACK_ERR_UNSUPPORTED;  // prefill reads cached sums
   if (batch > kMaxGridYZ) return HACK_ERR_UNSUPPORTED;  // one grid plane per sequence
   const int64_t cap = cache_capacity(layout, cache, batch);
   if (cap < 0) return HACK_ERR_INVALID_ARGUMENT;
@@ -271,6 +281,7 @@ hack_status hack_debug_qk_products(const hack_kv_layout* layout, const hack_kv_c
   int64_t cap = 0;
   hack_status st = decode_common(layout, cache, q_dev, num_q_heads, seq_lens_dev, batch, max_len, a, &cap);
   if (st != HACK_OK) return st;
+  if (layout->sum_bytes == 0) return HACK_ERR_UNSUPPORTED;  // the exports read cached sums
   if (!q_codes_dev || !q_meta_dev || !products_dev) return HACK_ERR_INVALID_ARGUMENT;
   if (batch == 0) return HACK_OK;
   const hack::DecodePlan plan = hack::plan_decode(*layout, batch, num_q_heads, max_len);
@@ -292,6 +303,7 @@ hack_status hack_debug_pv_products(const hack_kv_layout* layout, const hack_kv_c
   // the query is not read in this mode; pass any non-null pointer through validation
   hack_status st = decode_common(layout, cache, p_codes_dev, num_q_heads, seq_lens_dev, batch, max_len, a, &cap);
   if (st != HACK_OK) return st;
+  if (layout->sum_bytes == 0) return HACK_ERR_UNSUPPORTED;  // the exports read cached sums
   if (!p_meta_dev || !products_dev || !out_dev) return HACK_ERR_INVALID_ARGUMENT;
   if (batch == 0) return HACK_OK;
   const int span = 4 * layout->partition;

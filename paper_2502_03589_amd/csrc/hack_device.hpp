@@ -51,6 +51,7 @@ __device__ __forceinline__ uint32_t load_sum(const uint8_t* base, int64_t idx, i
 }
 
 __device__ __forceinline__ void store_sum(uint8_t* base, int64_t idx, int sum_bytes, uint32_t v) {
+  if (sum_bytes == 0) return;  // no cached sums (summation elimination off)
   if (sum_bytes == 1) base[idx] = (uint8_t)v;
   else reinterpret_cast<uint16_t*>(base)[idx] = (uint16_t)v;
 }

@@ -62,6 +62,23 @@ __device__ __forceinline__ v4i unpack16(const uint32_t* w) {
   }
 }
 
+// Sum of the b-bit codes packed in N dwords, from population counts of the bit
+// planes (the sum a cache without summation elimination does not store).
+template <int BITS, int N>
+__device__ __forceinline__ uint32_t code_sum(const uint32_t* w) {
+  uint32_t s = 0;
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    if constexpr (BITS == 2) {
+      s += __popc(w[i] & 0x55555555u) + 2u * __popc(w[i] & 0xAAAAAAAAu);
+    } else {
+      s += __popc(w[i] & 0x11111111u) + 2u * __popc(w[i] & 0x22222222u) + 4u * __popc(w[i] & 0x44444444u) +
+           8u * __popc(w[i] & 0x88888888u);
+    }
+  }
+  return s;
+}
+
 // N dwords from a 4*N-byte aligned address, as wide as the count allows.
 template <int N>
 __device__ __forceinline__ void load_words(const uint8_t* p, uint32_t* w) {
@@ -323,7 +340,9 @@ __device__ __forceinline__ void merge_chunks(const DecodeArgs& a, int s, int hkv
   }
 }
 
-template <int BITS, int PI, int GT, int MODE, int QP>
+// SE: the cache stores the partition code sums (summation elimination, Sec. 5.3);
+// without them each sum is rebuilt from the packed codes already in registers.
+template <int BITS, int PI, int GT, int MODE, int QP, bool SE>
 __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decode_kernel(DecodeArgs a) {
   constexpr int D = 128;
   // Q and P codes of QP bits: 2^QP - 1 levels; they enter the signed MFMA as code - 2^(QP-1)
@@ -526,7 +545,8 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
       if (full || span0 + 16 * ti + col < L) {
         load_words<KW>(b.kc + o_kc + ti * 16 * KROW, d.kc[ti]);
         d.km[ti] = *reinterpret_cast<const uint32_t*>(b.km + o_km + ti * 16 * P * 4);
-        if constexpr (SB == 1) d.kz[ti] = b.kz[o_kz + ti * 16 * P];
+        if constexpr (!SE) d.kz[ti] = 0u;
+        else if constexpr (SB == 1) d.kz[ti] = b.kz[o_kz + ti * 16 * P];
         else d.kz[ti] = *reinterpret_cast<const uint16_t*>(b.kz + o_kz + ti * 16 * P * 2);
       } else {
 #pragma unroll
@@ -550,7 +570,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
 #pragma unroll
         for (int i = 0; i < 2; ++i) lds_dma16(b.vm + o_vm + 16 * i, wl.vst[0].meta[i]);
 #pragma unroll
-        for (int i = 0; i < VS::NZ; ++i) {
+        for (int i = 0; i < (SE ? VS::NZ : 0); ++i) {
           if constexpr (VS::ZB == 4) lds_dma4(b.vz + o_vz + 4 * i, wl.vst[0].sums[i]);
           else lds_dma16(b.vz + o_vz + 16 * i, wl.vst[0].sums[i]);
         }
@@ -558,7 +578,12 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
     } else if (gvalid) {
       load_words<8 * VW>(b.vc + o_vc, d.vc);
       load_words<8>(b.vm + o_vm, d.vm);
-      load_words<2 * SB>(b.vz + o_vz, d.vz);
+      if constexpr (SE) {
+        load_words<2 * SB>(b.vz + o_vz, d.vz);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 2 * SB; ++j) d.vz[j] = 0u;
+      }
     } else {
 #pragma unroll
       for (int w = 0; w < 8 * VW; ++w) d.vc[w] = 0u;
@@ -631,7 +656,14 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
           const v4i b1 = unpack16<BITS>(d.kc[ti] + SW);
           // the lane's own K partition: m_k, s_k and the cached code sum
           const float mk = lo_half(d.km[ti]), skv = hi_half(d.km[ti]);
-          const float bz = skv * (float)d.kz[ti];
+          uint32_t kzv;  // code sum of the lane's K partition
+          if constexpr (SE) {
+            kzv = d.kz[ti];
+          } else {
+            kzv = code_sum<BITS, KW>(d.kc[ti]);
+            if constexpr (QPP == 2) kzv += (uint32_t)__shfl_xor((int)kzv, 16, 64);  // the partition's other quarter
+          }
+          const float bz = skv * (float)kzv;
 #pragma unroll
           for (int rt = 0; rt < GT; ++rt) {
             v4i acc = v4i{0, 0, 0, 0};
@@ -810,7 +842,8 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
       for (int j = 0; j < 8; ++j) {
         const float mv = lo_half(vmr[j]), svj = hi_half(vmr[j]);
         uint32_t zj;
-        if constexpr (SB == 1) zj = (vzr[j >> 2] >> (8 * (j & 3))) & 0xFFu;
+        if constexpr (!SE) zj = code_sum<BITS, VW>(vcr + j * VW);
+        else if constexpr (SB == 1) zj = (vzr[j >> 2] >> (8 * (j & 3))) & 0xFFu;
         else zj = (vzr[j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
         const float vbar = fmaf(n_g, mv, svj * (float)zj);  // s_v sum v' + n m_v
 #pragma unroll
@@ -1034,10 +1067,10 @@ DecodePlan plan_decode(const hack_kv_layout& lay, int batch, int num_q_heads, in
   return p;
 }
 
-template <int BITS, int PI, int GT, int MODE, int QP>
+template <int BITS, int PI, int GT, int MODE, int QP, bool SE>
 static hipError_t decode_impl(const DecodeArgs& a, int batch, hipStream_t stream) {
   dim3 grid((unsigned)(a.c.kv_heads * a.head_groups), (unsigned)batch, (unsigned)a.splits);
-  hipLaunchKernelGGL((decode_kernel<BITS, PI, GT, MODE, QP>), grid, dim3(256), 0, stream, a);
+  hipLaunchKernelGGL((decode_kernel<BITS, PI, GT, MODE, QP, SE>), grid, dim3(256), 0, stream, a);
   if (MODE == MODE_ATTEND && a.splits > 1 && !HACK_DECODE_FUSED_MERGE)
     hipLaunchKernelGGL(decode_merge_kernel, dim3((unsigned)a.c.kv_heads, (unsigned)batch), dim3(256), 0, stream, a);
   return hipGetLastError();
@@ -1045,10 +1078,13 @@ static hipError_t decode_impl(const DecodeArgs& a, int batch, hipStream_t stream
 
 template <int BITS, int PI, int GT, int QP>
 static hipError_t decode_mode(const DecodeArgs& a, int batch, int mode, hipStream_t stream) {
+  if (a.c.sum_bytes == 0)  // no cached sums: attention only (the exports need them)
+    return mode == MODE_ATTEND ? decode_impl<BITS, PI, GT, MODE_ATTEND, QP, false>(a, batch, stream)
+                               : hipErrorInvalidValue;
   switch (mode) {
-    case MODE_ATTEND: return decode_impl<BITS, PI, GT, MODE_ATTEND, QP>(a, batch, stream);
-    case MODE_QK: return decode_impl<BITS, PI, GT, MODE_QK, QP>(a, batch, stream);
-    case MODE_PV: return decode_impl<BITS, PI, GT, MODE_PV, QP>(a, batch, stream);
+    case MODE_ATTEND: return decode_impl<BITS, PI, GT, MODE_ATTEND, QP, true>(a, batch, stream);
+    case MODE_QK: return decode_impl<BITS, PI, GT, MODE_QK, QP, true>(a, batch, stream);
+    case MODE_PV: return decode_impl<BITS, PI, GT, MODE_PV, QP, true>(a, batch, stream);
     default: return hipErrorInvalidValue;
   }
 }

@@ -101,7 +101,7 @@ __global__ __launch_bounds__(256) void quantize_v_kernel(CacheView c, const __ha
   *reinterpret_cast<uint2*>(reinterpret_cast<uint32_t*>(c.v_meta) + vb * d + ch) = uint2{meta[0], meta[1]};
   if (c.sum_bytes == 1) {
     *reinterpret_cast<uint16_t*>(c.v_sums + vb * d + ch) = (uint16_t)(sums[0] | (sums[1] << 8));
-  } else {
+  } else if (c.sum_bytes == 2) {
     *reinterpret_cast<uint32_t*>(c.v_sums + 2 * (vb * d + ch)) = sums[0] | (sums[1] << 16);
   }
   if (blk == F) {  // the open block: keep its fp16 originals

@@ -55,6 +55,7 @@ _LAY = ctypes.POINTER(hack_kv_layout)
 _CAC = ctypes.POINTER(hack_kv_cache)
 _SIGS = {
     "hack_kv_layout_make": (_I32, [_LAY, _I32, _I32, _I32, _I32, _I32, _I32, _I32, ctypes.c_uint64]),
+    "hack_kv_layout_set_sums": (_I32, [_LAY, _I32]),
     "hack_kv_bytes": (_I64, [_LAY, _I64, _I32]),
     "hack_quantize": (_I32, [_LAY, _CAC, _P, _P, _P, _I32, _I32, _P]),
     "hack_append": (_I32, [_LAY, _CAC, _P, _P, _P, _I32, _I32, _I32, _P]),
@@ -111,11 +112,19 @@ def hack_status_string(status: int) -> str:
 
 def hack_kv_layout_make(head_dim: int, num_kv_heads: int, kv_bits: int, partition: int,
                         page_tokens: int, qp_bits: int = 8, rounding: int = ROUND_NEAREST_EVEN,
-                        seed: int = 0) -> hack_kv_layout:
+                        seed: int = 0, sums_cached: bool = True) -> hack_kv_layout:
+    """A validated layout; sums_cached=False turns summation elimination off
+    (hack_kv_layout_set_sums): no code sums are stored and decode rebuilds them."""
     out = hack_kv_layout()
     _check(lib().hack_kv_layout_make(ctypes.byref(out), head_dim, num_kv_heads, kv_bits, partition,
                                      page_tokens, qp_bits, rounding, seed), "hack_kv_layout_make")
+    if not sums_cached:
+        hack_kv_layout_set_sums(out, False)
     return out
+
+
+def hack_kv_layout_set_sums(layout: hack_kv_layout, cached: bool) -> None:
+    _check(lib().hack_kv_layout_set_sums(ctypes.byref(layout), 1 if cached else 0), "hack_kv_layout_set_sums")
 
 
 def hack_kv_bytes(layout: hack_kv_layout, count: int, section: int) -> int:

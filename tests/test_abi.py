@@ -170,3 +170,38 @@ def test_status_strings(lib):
     for st in range(6):
         assert len(hk.hack_status_string(st)) > 0
     assert hk.hack_status_string(99) == "unknown status"
+
+
+@pytest.mark.parametrize("bits,pi", [(2, 32), (4, 64), (2, 128)])
+def test_summation_elimination_off_layout(lib, bits, pi):
+    """Sums not cached (Sec. 5.3's summation elimination switched off): the sum sections
+    have no bytes, every other section is unchanged, and it can be switched back."""
+    d, H, pt, pages = 128, 8, 256, 3
+    on = hk.hack_kv_layout_make(d, H, bits, pi, pt)
+    off = hk.hack_kv_layout_make(d, H, bits, pi, pt, sums_cached=False)
+    assert off.sum_bytes == 0 and on.sum_bytes == O.sum_bytes(bits, pi)
+    for sec in range(7):
+        want = 0 if sec in (hk.K_SUMS, hk.V_SUMS) else hk.hack_kv_bytes(on, pages, sec)
+        assert hk.hack_kv_bytes(off, pages, sec) == want
+    hk.hack_kv_layout_set_sums(off, True)
+    assert off.sum_bytes == on.sum_bytes
+    assert lib.hack_kv_layout_set_sums(ctypes.byref(off), 2) == 1
+    assert lib.hack_kv_layout_set_sums(None, 0) == 1
+
+
+def test_summation_elimination_off_arguments(lib):
+    """Without cached sums the sum pointers may be null; prefill and the debug exports
+    (which read the cached sums) report UNSUPPORTED before any launch."""
+    lay = hk.hack_kv_layout_make(128, 2, 2, 32, 128, sums_cached=False)
+    L = ctypes.byref(lay)
+    fake = _Fake(pages=4)
+    fake.struct.k_sums = None
+    fake.struct.v_sums = None
+    C = ctypes.byref(fake.struct)
+    p = ctypes.c_void_p(0x5000)
+    assert lib.hack_attend_prefill(L, C, p, 8, 2, 100, 1, p, None) == 2
+    assert lib.hack_debug_qk_products(L, C, p, 8, p, 2, 100, p, p, p, None) == 2
+    assert lib.hack_debug_pv_products(L, C, p, p, 8, p, 2, 100, p, p, None) == 2
+    assert lib.hack_quantize(L, C, p, p, p, 2, 129, None) == 3  # validated (capacity), not rejected
+    on = hk.hack_kv_layout_make(128, 2, 2, 32, 128)
+    assert lib.hack_quantize(ctypes.byref(on), C, p, p, p, 2, 10, None) == 1  # cached sums need pointers
