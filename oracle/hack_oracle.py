@@ -52,6 +52,8 @@ TAIL_FP16 = 0
 TAIL_REQUANT = 1
 STREAM_K = 1
 STREAM_V = 2
+STREAM_Q = 3
+STREAM_P = 4
 
 _GOLDEN = np.uint64(0x9E3779B97F4A7C15)
 _MIX1 = np.uint64(0xBF58476D1CE4E5B9)
@@ -84,6 +86,29 @@ def stochastic_threshold(seed: int, stream: int, idx) -> np.ndarray:
     key = np.uint64(seed) ^ (np.uint64(stream) << np.uint64(56))
     h = splitmix64(np.asarray(idx, dtype=np.uint64) ^ key)
     return (h >> np.uint64(40)).astype(np.float32) * np.float32(2.0 ** -24)
+
+
+def qp_index(seq: int, q_heads: int, head: int, row, col):
+    """Canonical index of a transient Q or P element (reading R4): query head `head` of
+    sequence `seq`, query row `row` (0 in decode), column `col` (channel of Q, key token
+    of P): ((seq*H_q + head) * 2^20 + row) * 2^24 + col."""
+    with np.errstate(over="ignore"):
+        base = (np.uint64(seq * q_heads + head) << np.uint64(20)) + np.asarray(row, dtype=np.uint64)
+        return (base << np.uint64(24)) + np.asarray(col, dtype=np.uint64)
+
+
+@dataclasses.dataclass
+class QPStochastic:
+    """Stochastic rounding of the Q and P codes of one query row (reading R4): the
+    thresholds of stream STREAM_Q (Q channels) and STREAM_P (P key tokens)."""
+    seed: int
+    seq: int
+    q_heads: int
+    head: int
+    row: int = 0
+
+    def u(self, stream: int, cols) -> np.ndarray:
+        return stochastic_threshold(self.seed, stream, qp_index(self.seq, self.q_heads, self.head, self.row, cols))
 
 
 # ----------------------------------------------------------------------------
@@ -292,23 +317,28 @@ def dequantize_v_blocks(sq: SeqKV) -> np.ndarray:
 # ----------------------------------------------------------------------------
 # Attention on quantized operands (Sec. 5.3 with Eq. 2-4)
 # ----------------------------------------------------------------------------
-def quantize_query(q, partition: int, bits: int = 8):
-    """Q row quantized per partition along d with float32 metadata (Sec. 5.1: Q uses 8 bits)."""
+def quantize_query(q, partition: int, bits: int = 8, sr: Optional[QPStochastic] = None):
+    """Q row quantized per partition along d with float32 metadata (Sec. 5.1: Q uses 8 bits);
+    rounded to nearest, or stochastically with the thresholds of `sr`."""
     q = np.asarray(q, np.float16)
     d = q.shape[0]
     P = d // partition
-    c, m, s, tot = quantize_partition(q.reshape(P, partition), bits, "f32")
+    if sr is None:
+        c, m, s, tot = quantize_partition(q.reshape(P, partition), bits, "f32")
+    else:
+        u = sr.u(STREAM_Q, np.arange(d)).reshape(P, partition)
+        c, m, s, tot = quantize_partition(q.reshape(P, partition), bits, "f32", STOCHASTIC, u)
     return c.reshape(d), m.astype(np.float64), s.astype(np.float64), tot
 
 
-def scores(q, sq: SeqKV, qp_bits: int = 8, upto: Optional[int] = None):
+def scores(q, sq: SeqKV, qp_bits: int = 8, upto: Optional[int] = None, sr: Optional[QPStochastic] = None):
     """S_j = (1/sqrt(d)) sum_p Eq4(q'_p, k'_{j,p}) for j < upto, using the cached K sums.
     Returns (S float64 [upto], integer products int64 [upto][P], q codes, q min, q scale)."""
     d = sq.k_codes.shape[1]
     Pi = sq.partition
     P = d // Pi
     L = sq.length if upto is None else upto
-    qc, qm, qs, qsum = quantize_query(q, Pi, qp_bits)
+    qc, qm, qs, qsum = quantize_query(q, Pi, qp_bits, sr)
     S = np.zeros(L)
     prods = np.zeros((L, P), np.int64)
     for p in range(P):
@@ -322,7 +352,14 @@ def scores(q, sq: SeqKV, qp_bits: int = 8, upto: Optional[int] = None):
     return S, prods, qc, qm, qs
 
 
-def pv_blocks(prob, sq: SeqKV, qp_bits: int, tail_mode: int):
+def _quantize_p(p, qp_bits: int, sr: Optional[QPStochastic], first: int):
+    """One V block's probabilities (key tokens first, first+1, ...) quantized in float64."""
+    if sr is None:
+        return quantize_partition(p, qp_bits, "f64")
+    return quantize_partition(p, qp_bits, "f64", STOCHASTIC, sr.u(STREAM_P, first + np.arange(len(p))))
+
+
+def pv_blocks(prob, sq: SeqKV, qp_bits: int, tail_mode: int, sr: Optional[QPStochastic] = None):
     """O_c = sum over V blocks of Eq4(P'_block, V'_block,c) plus the open block
     (fp16 and unquantized P in TAIL_FP16 mode; re-quantized with n=T in TAIL_REQUANT mode)."""
     d = sq.k_codes.shape[1]
@@ -330,7 +367,7 @@ def pv_blocks(prob, sq: SeqKV, qp_bits: int, tail_mode: int):
     F, T = sq.full_blocks, sq.tail_tokens
     O = np.zeros(d)
     for blk in range(F):
-        pc, pm, ps, psum = quantize_partition(prob[blk * Pi:(blk + 1) * Pi], qp_bits, "f64")
+        pc, pm, ps, psum = _quantize_p(prob[blk * Pi:(blk + 1) * Pi], qp_bits, sr, blk * Pi)
         D = pc @ sq.v_codes[blk]                      # int64 [d]
         O += ps * sq.v_scale[blk] * D + ps * sq.v_min[blk] * psum \
             + pm * sq.v_scale[blk] * sq.v_sum[blk] + Pi * pm * sq.v_min[blk]
@@ -339,7 +376,7 @@ def pv_blocks(prob, sq: SeqKV, qp_bits: int, tail_mode: int):
         if tail_mode == TAIL_FP16:
             O += pt @ sq.v_tail.astype(np.float64)
         else:
-            pc, pm, ps, psum = quantize_partition(pt, qp_bits, "f64")
+            pc, pm, ps, psum = _quantize_p(pt, qp_bits, sr, F * Pi)
             D = pc @ sq.v_codes[F, :T]
             O += ps * sq.v_scale[F] * D + ps * sq.v_min[F] * psum \
                 + pm * sq.v_scale[F] * sq.v_sum[F] + T * pm * sq.v_min[F]
@@ -352,46 +389,52 @@ def softmax(S):
     return e / e.sum()
 
 
-def decode_row(q, sq: SeqKV, qp_bits: int = 8, tail_mode: int = TAIL_FP16):
+def decode_row(q, sq: SeqKV, qp_bits: int = 8, tail_mode: int = TAIL_FP16, sr: Optional[QPStochastic] = None):
     """One decode query row over the whole cached sequence (Sec. 5.3, L_Q = 1)."""
     if sq.length == 0:
         return np.zeros(sq.k_codes.shape[1])
-    S, _, _, _, _ = scores(q, sq, qp_bits)
-    return pv_blocks(softmax(S), sq, qp_bits, tail_mode)
+    S, _, _, _, _ = scores(q, sq, qp_bits, sr=sr)
+    return pv_blocks(softmax(S), sq, qp_bits, tail_mode, sr)
 
 
-def prefill_row(q, sq: SeqKV, i: int, causal: bool, qp_bits: int = 8):
+def prefill_row(q, sq: SeqKV, i: int, causal: bool, qp_bits: int = 8, sr: Optional[QPStochastic] = None):
     """Prefill row i (L_Q = L_KV, Sec. 5.3): causal rows see tokens j <= i; P is zero
     past i and its blocks are quantized over all Pi entries (reading R7)."""
     L = sq.length
     upto = i + 1 if causal else L
-    S, _, _, _, _ = scores(q, sq, qp_bits, upto)
+    S, _, _, _, _ = scores(q, sq, qp_bits, upto, sr)
     prob = np.zeros(L)
     prob[:upto] = softmax(S)
-    return pv_blocks(prob, sq, qp_bits, TAIL_FP16)
+    return pv_blocks(prob, sq, qp_bits, TAIL_FP16, sr)
 
 
-def attend_decode(q, seqs, kv_heads: int, qp_bits: int = 8, tail_mode: int = TAIL_FP16, rows=None):
+def attend_decode(q, seqs, kv_heads: int, qp_bits: int = 8, tail_mode: int = TAIL_FP16, rows=None,
+                  stochastic_seed: Optional[int] = None):
     """q [B][H_q][d] fp16; seqs[b][h_kv] SeqKV.  Returns O float32 [B][H_q][d].
-    `rows` optionally restricts the work to a list of (b, h_q) pairs (others stay 0)."""
+    `rows` optionally restricts the work to a list of (b, h_q) pairs (others stay 0).
+    With `stochastic_seed`, Q and P codes are rounded stochastically (reading R4)."""
     B, Hq, d = q.shape
     G = Hq // kv_heads
     O = np.zeros((B, Hq, d), np.float64)
     todo = rows if rows is not None else [(b, h) for b in range(B) for h in range(Hq)]
     for b, h in todo:
-        O[b, h] = decode_row(q[b, h], seqs[b][h // G], qp_bits, tail_mode)
+        sr = None if stochastic_seed is None else QPStochastic(stochastic_seed, b, Hq, h, 0)
+        O[b, h] = decode_row(q[b, h], seqs[b][h // G], qp_bits, tail_mode, sr)
     return O.astype(np.float32)
 
 
-def attend_prefill(Q, seqs, kv_heads: int, causal: bool = True, qp_bits: int = 8, rows=None):
+def attend_prefill(Q, seqs, kv_heads: int, causal: bool = True, qp_bits: int = 8, rows=None,
+                   stochastic_seed: Optional[int] = None):
     """Q [B][H_q][L][d] fp16.  Returns O float32 [B][H_q][L][d].
-    `rows` optionally restricts the work to a list of (b, h_q, i) triples."""
+    `rows` optionally restricts the work to a list of (b, h_q, i) triples.
+    With `stochastic_seed`, Q and P codes are rounded stochastically (reading R4)."""
     B, Hq, L, d = Q.shape
     G = Hq // kv_heads
     O = np.zeros((B, Hq, L, d), np.float64)
     todo = rows if rows is not None else [(b, h, i) for b in range(B) for h in range(Hq) for i in range(L)]
     for b, h, i in todo:
-        O[b, h, i] = prefill_row(Q[b, h, i], seqs[b][h // G], i, causal, qp_bits)
+        sr = None if stochastic_seed is None else QPStochastic(stochastic_seed, b, Hq, h, i)
+        O[b, h, i] = prefill_row(Q[b, h, i], seqs[b][h // G], i, causal, qp_bits, sr)
     return O.astype(np.float32)
 
 

@@ -271,8 +271,8 @@ def test_planted_score_mistakes_are_caught(monkeypatch):
     ref = _dequant_scores(q, sq)
     real = O.quantize_query
 
-    def wrong_sum(qrow, pi, bits=8):
-        c, m, s, tot = real(qrow, pi, bits)
+    def wrong_sum(qrow, pi, bits=8, sr=None):
+        c, m, s, tot = real(qrow, pi, bits, sr)
         return c, m, s, tot[::-1].copy()           # sums of the wrong partitions
     monkeypatch.setattr(O, "quantize_query", wrong_sum)
     S, _, _, _, _ = O.scores(q, sq)
@@ -308,3 +308,58 @@ def test_empty_sequence_packs_and_attends():
     out = O.pack_cache([[sq]], 1, 128, 2, 32, 64, 1)
     assert not out["k_codes"].any() and not out["v_tail"].any()
     assert np.all(O.decode_row(_f16(3, (128,)), sq) == 0)
+
+
+# ---- stochastic rounding of the transient Q and P codes (reading R4) ----------------
+def test_qp_index_layout_and_distinctness():
+    """((seq*H_q + head) * 2^20 + row) * 2^24 + col: the closed form, and distinct values
+    over a small grid of (seq, head, row, col) by brute force."""
+    assert int(O.qp_index(1, 4, 2, 3, 5)) == ((1 * 4 + 2) * 2 ** 20 + 3) * 2 ** 24 + 5
+    seen = set()
+    for b in range(3):
+        for h in range(4):
+            for i in range(3):
+                cols = O.qp_index(b, 4, h, i, np.arange(300))
+                seen.update(int(x) for x in cols)
+    assert len(seen) == 3 * 4 * 3 * 300
+
+
+def test_stochastic_query_codes_are_floor_or_ceil_and_unbiased():
+    """Over 4000 seeds each Q code is floor(t) or floor(t)+1 with t = (x-m)*fl(1/s) in
+    float32 (R3), and the mean dequantized value s*c + m approaches x (E[c] = t)."""
+    q = _f16(21, (128,))
+    n = 4000
+    acc = np.zeros(128)
+    c0, m0, s0, _ = O.quantize_query(q, 32)              # nearest: same m, s
+    x = q.astype(np.float32).reshape(4, 32)
+    t = (x - m0[:, None].astype(np.float32)) * (np.float32(1) / s0[:, None].astype(np.float32))
+    fl = np.floor(t).reshape(128)
+    for seed in range(n):
+        c, m, s, _ = O.quantize_query(q, 32, 8, O.QPStochastic(seed, 0, 1, 0, 0))
+        assert np.array_equal(m, m0) and np.array_equal(s, s0)
+        assert np.all((c == fl) | (c == fl + 1))
+        acc += np.repeat(s, 32) * c + np.repeat(m, 32)
+    mean = acc / n
+    sigma = np.repeat(s0, 32) / 2 / math.sqrt(n)          # |c - t| < 1, so sd(s c) <= s/2
+    assert np.all(np.abs(mean - q.astype(np.float64)) <= 5 * sigma + 1e-12)
+
+
+def test_stochastic_p_blocks_are_unbiased():
+    """For a fixed probability row, the mean over seeds of the Eq. 4 output of the
+    stochastically quantized P blocks approaches p . V_hat (the dequantized V blocks) plus
+    the fp16 open block: the closed form of unbiased rounding."""
+    _, _, sq = _seq(41, 3 * 32 + 9, 2, 32)
+    g = np.random.default_rng(5)
+    prob = g.random(sq.length)
+    prob /= prob.sum()
+    vhat = np.concatenate([sq.v_codes[k] * sq.v_scale[k][None, :] + sq.v_min[k][None, :]
+                           for k in range(sq.full_blocks)])
+    exact = prob[:vhat.shape[0]] @ vhat + prob[vhat.shape[0]:] @ sq.v_tail.astype(np.float64)
+    n = 1500
+    outs = np.stack([O.pv_blocks(prob, sq, 8, O.TAIL_FP16, O.QPStochastic(seed, 0, 1, 0, 0)) for seed in range(n)])
+    near = O.pv_blocks(prob, sq, 8, O.TAIL_FP16)
+    # spread of one call around the exact value: at most one code step s_p per element
+    bound = 5 * outs.std(axis=0) / math.sqrt(n) + 1e-12
+    assert np.all(np.abs(outs.mean(axis=0) - exact) <= bound)
+    assert not np.allclose(outs[0], outs[1])             # different seeds, different codes
+    assert np.abs(near - exact).max() > 0                # nearest rounding is not the closed form
