@@ -275,12 +275,14 @@ def main():
         result["prefill"] = bench_prefill(args.prefill_iters)
         # the same workload with 4-bit Q/P codes (the literal reading of its 4-bit Q/K/V/P)
         result["prefill_qp4"] = bench_prefill(max(3, args.prefill_iters // 2), 4)
+        # the paper's rounding: stochastic K/V, Q and P codes
+        result["prefill_stochastic"] = bench_prefill(max(3, args.prefill_iters // 2), 8, 1)
     if not args.no_cpu_baseline and args.only is None:
         result["cpu_baseline"] = cpu_baseline_decode(wl)
     print(json.dumps(result), flush=True)
 
 
-def bench_prefill(iters: int, qp_bits: int = 8):
+def bench_prefill(iters: int, qp_bits: int = 8, rounding: int = 0):
     """Causal prefill (batch 1, 32/8 heads, 8192 tokens, 4-bit K/V, partition 64, Q/P
     codes of qp_bits bits): quantize-on-write of the prompt's K/V then attention; int8
     ops of the causal triangle = 2 products x 32 heads x L(L+1)/2 x 128 x 2."""
@@ -290,7 +292,7 @@ def bench_prefill(iters: int, qp_bits: int = 8):
     wl = synth.WORKLOADS["prefill_l8192"]
     B, Hq, H, d, L = wl.batch, wl.q_heads, wl.kv_heads, wl.head_dim, wl.context
     dev = torch.device("cuda:0")
-    lay = hk.hack_kv_layout_make(d, H, wl.kv_bits, wl.partition, L, qp_bits)
+    lay = hk.hack_kv_layout_make(d, H, wl.kv_bits, wl.partition, L, qp_bits, rounding, wl.seed)
     c = hk.KVCache(lay, B, B, None, dev)
     k = torch.from_numpy(synth.normal_f16(wl.seed, "k", (B, H, L, d))).to(dev)
     v = torch.from_numpy(synth.normal_f16(wl.seed, "v", (B, H, L, d))).to(dev)
@@ -319,7 +321,8 @@ def bench_prefill(iters: int, qp_bits: int = 8):
     q_ms = float(np.median(qt))
     tops = ops / (a_ms * 1e-3) / 1e12
     q_gbs = quantize_bytes(B, H, L, d, wl.kv_bits, wl.partition, lay.sum_bytes) / (q_ms * 1e-3) / 1e9
-    return {"workload": "prefill_l8192", "qp_bits": qp_bits, "int8_ops": ops, "attend_ms": round(a_ms, 4),
+    return {"workload": "prefill_l8192", "qp_bits": qp_bits, "rounding": "stochastic" if rounding else "nearest",
+            "int8_ops": ops, "attend_ms": round(a_ms, 4),
             "quantize_ms": round(q_ms, 4), "quantize_GBs": round(q_gbs, 1), "TOPS": round(tops, 2),
             "peak_TOPS": INT8_PEAK_TOPS, "frac": round(tops / INT8_PEAK_TOPS, 4)}
 
@@ -353,10 +356,12 @@ def bench_workload(name: str, steps: int, warmup: int):
         q = torch.from_numpy(synth.normal_f16(base.seed, "q", (B, Hq, d))).to(dev)
         ln = torch.full((B,), L, dtype=torch.int32, device=dev)
         R = 10
-        for bits, part, se in ((2, 32, True), (2, 64, True), (4, 32, True), (4, 64, True),
-                               (2, 32, False), (2, 64, False), (4, 32, False), (4, 64, False)):
-            # se=False: summation elimination off, no cached sums (fewer bytes, sums rebuilt)
-            lay = hk.hack_kv_layout_make(d, H, bits, part, L, sums_cached=se)
+        for bits, part, se, rnd in ((2, 32, True, 0), (2, 64, True, 0), (4, 32, True, 0), (4, 64, True, 0),
+                                    (2, 32, False, 0), (2, 64, False, 0), (4, 32, False, 0), (4, 64, False, 0),
+                                    (2, 32, True, 1), (4, 64, True, 1)):
+            # se=False: summation elimination off, no cached sums (fewer bytes, sums rebuilt);
+            # rnd=1: stochastic rounding of K/V, Q and P codes
+            lay = hk.hack_kv_layout_make(d, H, bits, part, L, 8, rnd, base.seed, sums_cached=se)
             caches = [hk.KVCache(lay, B, B, None, dev) for _ in range(R)]
             for cache in caches:
                 hk.hack_quantize(lay, cache, k, v, ln, L)
@@ -375,6 +380,7 @@ def bench_workload(name: str, steps: int, warmup: int):
             ms = e0.elapsed_time(e1) / steps
             nbytes = B * H * decode_bytes_per_seq_head(L, d, bits, part, lay.sum_bytes) + B * Hq * d * 6
             print(json.dumps({"workload": name, "kv_bits": bits, "partition": part, "sums_cached": se,
+                              "rounding": "stochastic" if rnd else "nearest",
                               "metric": "decode GB/s",
                               "value": round(nbytes / ms / 1e6, 2), "unit": "GB/s", "us_per_call": round(ms * 1e3, 2),
                               "bytes_per_call": int(nbytes), "bytes_per_token_head": round(nbytes / (B * H * L), 2),

@@ -183,6 +183,9 @@ static hack_status decode_common(const hack_kv_layout* layout, const hack_kv_cac
   a.inv_qmax = 1.0f / a.qmax;
   a.qoff = 1 << (layout->qp_bits - 1);
   a.qoff_f = (float)a.qoff;
+  a.stochastic = layout->rounding == HACK_ROUND_STOCHASTIC;
+  a.key_q = layout->seed ^ (3ull << 56);
+  a.key_p = layout->seed ^ (4ull << 56);
   *cap_out = cap;
   return HACK_OK;
 }

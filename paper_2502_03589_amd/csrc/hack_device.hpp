@@ -71,6 +71,19 @@ __device__ __forceinline__ float sr_threshold(uint64_t key, uint64_t idx) {
   return (float)(uint32_t)(splitmix64(key ^ idx) >> 40) * 5.9604644775390625e-08f;
 }
 
+// Canonical index of a transient Q or P element: query head `head` of sequence `seq`,
+// query row `row` (0 in decode), column `col` (Q channel or P key token):
+// ((seq * H_q + head) * 2^20 + row) * 2^24 + col.
+__device__ __forceinline__ uint64_t qp_index(int seq, int q_heads, int head, int row, int col) {
+  return ((((uint64_t)(seq * q_heads + head)) << 20) + (uint64_t)row) * (1ull << 24) + (uint64_t)col;
+}
+
+// Stochastic rounding of t >= 0 to an integer code in [0, qmax]: floor(t) + [u < frac(t)].
+__device__ __forceinline__ float round_stochastic(float t, float u, float qmax) {
+  const float fl = floorf(t);
+  return fminf(fmaxf(fl + (u < t - fl ? 1.0f : 0.0f), 0.0f), qmax);
+}
+
 // Smallest fp16 value >= s (s >= 0, finite), as raw bits.
 __device__ __forceinline__ uint16_t half_bits_round_up(float s) {
   __half h = __float2half_rn(s);

@@ -60,6 +60,7 @@ struct DecodeArgs {
   int capacity;
   int stochastic;
   uint64_t key_k, key_v;
+  uint64_t key_q, key_p;  // stochastic rounding of the Q and P codes (streams 3 and 4)
   // test exports
   uint8_t* dbg_qcodes;    // [B][H_q][128]
   float* dbg_qmeta;       // [B][H_q][P][2]

@@ -342,7 +342,8 @@ __device__ __forceinline__ void merge_chunks(const DecodeArgs& a, int s, int hkv
 
 // SE: the cache stores the partition code sums (summation elimination, Sec. 5.3);
 // without them each sum is rebuilt from the packed codes already in registers.
-template <int BITS, int PI, int GT, int MODE, int QP, bool SE>
+// SR: the Q and P codes are rounded stochastically (the layout's rounding mode).
+template <int BITS, int PI, int GT, int MODE, int QP, bool SE, bool SR>
 __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decode_kernel(DecodeArgs a) {
   constexpr int D = 128;
   // Q and P codes of QP bits: 2^QP - 1 levels; they enter the signed MFMA as code - 2^(QP-1)
@@ -453,8 +454,14 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
         sq = __fdiv_rn(__fsub_rn(mx, mn), kQmax);
         if (sq != 0.0f) {
           const float r = __fdiv_rn(1.0f, sq);
-          c0 = fminf(rintf(__fmul_rn(__fsub_rn(x0, mn), r)), kQmax);
-          c1 = fminf(rintf(__fmul_rn(__fsub_rn(x1, mn), r)), kQmax);
+          const float t0 = __fmul_rn(__fsub_rn(x0, mn), r), t1 = __fmul_rn(__fsub_rn(x1, mn), r);
+          if constexpr (SR) {
+            c0 = round_stochastic(t0, sr_threshold(a.key_q, qp_index(s, Hq, hq, 0, 2 * lane)), kQmax);
+            c1 = round_stochastic(t1, sr_threshold(a.key_q, qp_index(s, Hq, hq, 0, 2 * lane + 1)), kQmax);
+          } else {
+            c0 = fminf(rintf(t0), kQmax);
+            c1 = fminf(rintf(t1), kQmax);
+          }
         }
       }
       int csum = (int)c0 + (int)c1;
@@ -732,7 +739,14 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
 #pragma unroll
             for (int tl = 0; tl < TILES; ++tl) {
               // round-to-nearest-even with saturation (codes stay within [0, qmax])
-              const uint32_t code = __builtin_amdgcn_cvt_pk_u8_f32(fmaf(pt[tl], r, bias), 0, 0u);
+              uint32_t code;
+              if constexpr (SR) {
+                const int tok = bt0 + 16 * tl + col;
+                const float u = sr_threshold(a.key_p, qp_index(s, Hq, hkv * G + head0 + rt * 4 + grp, 0, tok));
+                code = (uint32_t)round_stochastic(fmaf(pt[tl], r, bias), u, kQmax);
+              } else {
+                code = __builtin_amdgcn_cvt_pk_u8_f32(fmaf(pt[tl], r, bias), 0, 0u);
+              }
               const bool valid = full || bt0 + 16 * tl + col < L;
               wl.p[rt][k][grp][tl * 16 + perm_position<BITS>(col)] = valid ? (int8_t)((int)code - kQoff) : (int8_t)0;
             }
@@ -1067,10 +1081,10 @@ DecodePlan plan_decode(const hack_kv_layout& lay, int batch, int num_q_heads, in
   return p;
 }
 
-template <int BITS, int PI, int GT, int MODE, int QP, bool SE>
+template <int BITS, int PI, int GT, int MODE, int QP, bool SE, bool SR = false>
 static hipError_t decode_impl(const DecodeArgs& a, int batch, hipStream_t stream) {
   dim3 grid((unsigned)(a.c.kv_heads * a.head_groups), (unsigned)batch, (unsigned)a.splits);
-  hipLaunchKernelGGL((decode_kernel<BITS, PI, GT, MODE, QP, SE>), grid, dim3(256), 0, stream, a);
+  hipLaunchKernelGGL((decode_kernel<BITS, PI, GT, MODE, QP, SE, SR>), grid, dim3(256), 0, stream, a);
   if (MODE == MODE_ATTEND && a.splits > 1 && !HACK_DECODE_FUSED_MERGE)
     hipLaunchKernelGGL(decode_merge_kernel, dim3((unsigned)a.c.kv_heads, (unsigned)batch), dim3(256), 0, stream, a);
   return hipGetLastError();
@@ -1078,9 +1092,13 @@ static hipError_t decode_impl(const DecodeArgs& a, int batch, hipStream_t stream
 
 template <int BITS, int PI, int GT, int QP>
 static hipError_t decode_mode(const DecodeArgs& a, int batch, int mode, hipStream_t stream) {
-  if (a.c.sum_bytes == 0)  // no cached sums: attention only (the exports need them)
-    return mode == MODE_ATTEND ? decode_impl<BITS, PI, GT, MODE_ATTEND, QP, false>(a, batch, stream)
-                               : hipErrorInvalidValue;
+  if (a.c.sum_bytes == 0) {  // no cached sums: attention only (the exports need them)
+    if (mode != MODE_ATTEND) return hipErrorInvalidValue;
+    return a.stochastic ? decode_impl<BITS, PI, GT, MODE_ATTEND, QP, false, true>(a, batch, stream)
+                        : decode_impl<BITS, PI, GT, MODE_ATTEND, QP, false>(a, batch, stream);
+  }
+  if (a.stochastic && mode == MODE_ATTEND) return decode_impl<BITS, PI, GT, MODE_ATTEND, QP, true, true>(a, batch, stream);
+  if (a.stochastic && mode == MODE_QK) return decode_impl<BITS, PI, GT, MODE_QK, QP, true, true>(a, batch, stream);
   switch (mode) {
     case MODE_ATTEND: return decode_impl<BITS, PI, GT, MODE_ATTEND, QP, true>(a, batch, stream);
     case MODE_QK: return decode_impl<BITS, PI, GT, MODE_QK, QP, true>(a, batch, stream);

@@ -158,6 +158,7 @@ struct PrefillArgs {
   float inv_qmax;    // 1 / qmax
   int qoff;          // Q/P codes enter the signed int8 MFMA as code - qoff, qoff = 2^(b_QP - 1)
   float qoff_f;
+  uint64_t key_q, key_p;  // stochastic rounding of the Q and P codes (streams 3 and 4)
 };
 
 // Staging of one V block by the 512 threads of the workgroup (threads 0-255: K,
@@ -304,7 +305,8 @@ __device__ __forceinline__ void stage_store(const StageRegs<BITS, PI>& r, Stage<
 // workgroups' LDS, about 78 KB each for partition 64, fits the 160 KB of a CU), so
 // that one workgroup's block barrier and staging overlap the other's arithmetic
 // (measured 1.61 -> 1.36-1.44 ms on the 8K causal prefill).
-template <int BITS, int PI>
+// SR: the Q and P codes are rounded stochastically (the layout's rounding mode).
+template <int BITS, int PI, bool SR>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4))) void prefill_kernel(PrefillArgs a) {
   using C = PrefillCfg<PI>;
   using OP = Op<PI>;
@@ -368,7 +370,15 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const float t = __fmul_rn(__fsub_rn(x[4 * e4 + i], mn), r);
-            const int code = s32 != 0.0f ? (int)fminf(rintf(t), a.qmax) : 0;
+            int code = 0;
+            if (s32 != 0.0f) {
+              if constexpr (SR) {
+                const float u = sr_threshold(a.key_q, qp_index(s, a.num_q_heads, hq, row, c0 + 4 * e4 + i));
+                code = (int)round_stochastic(t, u, a.qmax);
+              } else {
+                code = (int)fminf(rintf(t), a.qmax);
+              }
+            }
             csum += code;
             v |= (uint32_t)((code - a.qoff) & 0xFF) << (8 * i);
           }
@@ -531,7 +541,16 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
       for (int tl = 0; tl < TL; ++tl) {
         uint32_t v = 0;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) v = __builtin_amdgcn_cvt_pk_u8_f32(fmaf(pt[tl][i], r, bias), i, v);
+        for (int i = 0; i < 4; ++i) {
+          if constexpr (SR) {
+            const int tok = tb0 + 16 * tl + 4 * grp + i;
+            const float u = sr_threshold(a.key_p, qp_index(s, a.num_q_heads, hq, row, tok));
+            const float c = round_stochastic(fmaf(pt[tl][i], r, -pmin * r), u, a.qmax);
+            v = __builtin_amdgcn_cvt_pk_u8_f32(c + (128.0f - a.qoff_f), i, v);
+          } else {
+            v = __builtin_amdgcn_cvt_pk_u8_f32(fmaf(pt[tl][i], r, bias), i, v);
+          }
+        }
         w[tl] = v ^ 0x80808080u;
       }
       const opT pop = OP::from(w);
@@ -638,9 +657,12 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
 }
 
 template <int BITS, int PI>
-static hipError_t prefill_impl(const PrefillArgs& a, int batch, hipStream_t stream) {
+static hipError_t prefill_impl(const PrefillArgs& a, int batch, bool stochastic, hipStream_t stream) {
   dim3 grid((unsigned)a.nqb, (unsigned)(a.c.kv_heads * a.head_groups), (unsigned)batch);
-  hipLaunchKernelGGL((prefill_kernel<BITS, PI>), grid, dim3(512), 0, stream, a);
+  if (stochastic)
+    hipLaunchKernelGGL((prefill_kernel<BITS, PI, true>), grid, dim3(512), 0, stream, a);
+  else
+    hipLaunchKernelGGL((prefill_kernel<BITS, PI, false>), grid, dim3(512), 0, stream, a);
   return hipGetLastError();
 }
 
@@ -656,15 +678,18 @@ hipError_t launch_prefill(const hack_kv_layout& lay, const CacheView& c, const _
   a.len = len;
   a.causal = causal;
   a.nqb = (len + kRows - 1) / kRows;
+  a.key_q = lay.seed ^ (3ull << 56);
+  a.key_p = lay.seed ^ (4ull << 56);
+  const bool sr = lay.rounding == HACK_ROUND_STOCHASTIC;
   a.qmax = (float)((1 << lay.qp_bits) - 1);
   a.inv_qmax = 1.0f / a.qmax;
   a.qoff = 1 << (lay.qp_bits - 1);
   a.qoff_f = (float)a.qoff;
   switch (lay.kv_bits * 1000 + lay.partition) {
-    case 2032: return prefill_impl<2, 32>(a, batch, stream);
-    case 2064: return prefill_impl<2, 64>(a, batch, stream);
-    case 4032: return prefill_impl<4, 32>(a, batch, stream);
-    case 4064: return prefill_impl<4, 64>(a, batch, stream);
+    case 2032: return prefill_impl<2, 32>(a, batch, sr, stream);
+    case 2064: return prefill_impl<2, 64>(a, batch, sr, stream);
+    case 4032: return prefill_impl<4, 32>(a, batch, sr, stream);
+    case 4064: return prefill_impl<4, 64>(a, batch, sr, stream);
     default: return hipErrorInvalidValue;
   }
 }

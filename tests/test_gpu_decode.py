@@ -225,3 +225,55 @@ def test_decode_step_equals_append_then_decode(bits, group, H, lens, tail_mode, 
 def synth_q(case, step):
     from paper_2502_03589_amd import synth
     return synth.normal_f16(case.seed + 1, "q", (case.batch, case.Hq, case.d), sub=step)
+
+
+@pytest.mark.parametrize("bits,pi,group,qp", [(2, 32, 4, 8), (4, 64, 8, 8), (2, 32, 2, 4)])
+def test_stochastic_query_codes_bit_exact(bits, pi, group, qp):
+    """With the layout's stochastic rounding the kernel draws the same SplitMix64
+    thresholds for the Q codes as the oracle: codes, metadata and products bit-exact."""
+    gu = _gpu()
+    from paper_2502_03589_amd import hack as hk
+    lens = [1, 47, 300]
+    gu.announce(f"stochastic qk products bits={bits} pi={pi} G={group} qp={qp}")
+    case = gu.Case(17 + bits, len(lens), 2, lens, bits, pi, group=group, rounding=O.STOCHASTIC,
+                   qp_bits=qp).quantize()
+    qc, qm, prod = hk.hack_debug_qk_products(case.layout, case.cache, torch.from_numpy(case.q).to(gu.DEV),
+                                             case.lens_dev, case.max_len)
+    torch.cuda.synchronize()
+    qc, qm, prod = qc.cpu().numpy(), qm.cpu().numpy(), prod.cpu().numpy()
+    seqs = case.oracle_seqs()
+    nearest_differs = False
+    for b in range(case.batch):
+        for h in range(case.Hq):
+            sr = O.QPStochastic(case.seed, b, case.Hq, h, 0)
+            S, prods, qcodes, qmin, qscale = O.scores(case.q[b, h], seqs[b][h // group], qp, sr=sr)
+            assert np.array_equal(qc[b, h], qcodes)
+            assert np.array_equal(qm[b, h, :, 0].astype(np.float64), qmin)
+            assert np.array_equal(qm[b, h, :, 1].astype(np.float64), qscale)
+            assert np.array_equal(prod[b, h, :lens[b]], prods)
+            nearest_differs |= not np.array_equal(O.quantize_query(case.q[b, h], pi, qp)[0], qcodes)
+    assert nearest_differs
+
+
+@pytest.mark.parametrize("bits,pi,group,H,lens,tail,qp", [
+    (2, 32, 4, 2, [256, 1, 31, 33, 300], 0, 8),
+    (4, 64, 8, 2, [77, 129, 1000], 1, 8),
+    (2, 32, 4, 1, [500, 65], 0, 4),
+])
+def test_stochastic_decode_matches_oracle(bits, pi, group, H, lens, tail, qp):
+    """Stochastic rounding of K/V (quantize), Q and P (attention) against the oracle
+    drawing the same thresholds."""
+    gu = _gpu()
+    from paper_2502_03589_amd import hack as hk
+    gu.announce(f"stochastic decode bits={bits} pi={pi} G={group} H={H} lens={lens} tail={tail} qp={qp}")
+    case = gu.Case(71 + bits + pi, len(lens), H, lens, bits, pi, group=group, rounding=O.STOCHASTIC,
+                   qp_bits=qp).quantize()
+    out = hk.hack_attend_decode(case.layout, case.cache, torch.from_numpy(case.q).to(gu.DEV), case.lens_dev,
+                                case.max_len, tail)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    ref = O.attend_decode(case.q, case.oracle_seqs(), H, qp, tail, stochastic_seed=case.seed)
+    err = gu.rel_err(got, ref)
+    near = O.attend_decode(case.q, case.oracle_seqs(), H, qp, tail)
+    print(f"max|d|/|O|inf = {err:.3e} (vs the nearest-rounding oracle: {gu.rel_err(got, near):.3e})")
+    assert err <= TOL

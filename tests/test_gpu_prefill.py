@@ -92,3 +92,18 @@ def test_prefill_last_row_matches_decode():
     torch.cuda.synchronize()
     d = dec.cpu().numpy()
     assert np.abs(d - got[:, :, L - 1, :]).max() <= TOL * np.abs(d).max()
+
+
+@pytest.mark.parametrize("bits,pi,group,H,L,causal,qp", [(4, 64, 4, 2, 200, True, 8), (2, 32, 8, 1, 131, False, 4)])
+def test_stochastic_prefill_matches_oracle(bits, pi, group, H, L, causal, qp):
+    """Stochastic rounding of K/V, Q and P in prefill against the oracle drawing the same
+    SplitMix64 thresholds."""
+    gu = _gpu()
+    gu.announce(f"stochastic prefill bits={bits} pi={pi} G={group} H={H} L={L} causal={causal} qp={qp}")
+    case = gu.Case(500 + bits + pi + L, 1, H, [L], bits, pi, group=group, rounding=O.STOCHASTIC,
+                   qp_bits=qp).quantize()
+    Q, got = _run_prefill(gu, case, causal)
+    ref = O.attend_prefill(Q, case.oracle_seqs(), H, causal=causal, qp_bits=qp, stochastic_seed=case.seed)
+    err = gu.rel_err(got, ref)
+    print(f"max|d|/|O|inf = {err:.3e}")
+    assert err <= TOL
