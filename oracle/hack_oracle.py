@@ -37,6 +37,10 @@ Readings where the paper is silent or garbled (each also listed in the design doc):
       other element.
   R8  grouped-query attention: q head h uses kv head h // (H_q / H_kv).
   R9  output is float32.
+  R15 the requantizing alternative to requantization elimination (Sec. 5.3): the
+      open V block keeps only codes; an append dequantizes them to fp16,
+      x_hat = fp16(fl(fl(s*c) + m)), adds the new value and quantizes the block again
+      with n = T + 1 (so the error of every earlier requantization is kept).
 """
 from __future__ import annotations
 
@@ -50,6 +54,7 @@ NEAREST_EVEN = 0
 STOCHASTIC = 1
 TAIL_FP16 = 0
 TAIL_REQUANT = 1
+TAIL_DEQUANT = 2
 STREAM_K = 1
 STREAM_V = 2
 STREAM_Q = 3
@@ -292,6 +297,55 @@ def quantize_sequence(k, v, bits: int, partition: int, rounding: int = NEAREST_E
         vcount[blk] = n
     return SeqKV(L, Pi, kc.reshape(L, d), km.astype(np.float64), ks.astype(np.float64), ksum,
                  vc, vm, vs, vsum, vcount, v[F * Pi:L].copy())
+
+
+def dequantize_to_f16(codes, m, s) -> np.ndarray:
+    """x_hat = fp16(fl32(fl32(s * c) + m)) (reading R15): float32 product, then sum,
+    then rounding to fp16 (the quantizer's inputs are fp16 values)."""
+    c = np.asarray(codes).astype(np.float32)
+    prod = (np.asarray(s, np.float32) * c).astype(np.float32)
+    return (prod + np.asarray(m, np.float32)).astype(np.float32).astype(np.float16)
+
+
+def append_requantizing(sq: SeqKV, k_row, v_row, bits: int, rounding: int = NEAREST_EVEN, seed: int = 0,
+                        seq: int = 0, head: int = 0, kv_heads: int = 1) -> SeqKV:
+    """Append token L = sq.length with the requantizing open block (reading R15): the
+    token's K partitions are quantized as usual; the open V block's codes are
+    dequantized to fp16, the new value is added and the block is quantized again with
+    n = T + 1 (a block that reaches Pi tokens is closed with those codes)."""
+    k_row = np.asarray(k_row, np.float16)
+    v_row = np.asarray(v_row, np.float16)
+    L, Pi = sq.length, sq.partition
+    d = k_row.shape[0]
+    P = d // Pi
+    uk = None
+    if rounding == STOCHASTIC:
+        uk = stochastic_threshold(seed, STREAM_K, element_index(seq, kv_heads, head, L, np.arange(d).reshape(P, Pi), d))
+    kc, km, ks, ksum = quantize_partition(k_row.reshape(P, Pi), bits, "f16", rounding, uk)
+    F, T = sq.full_blocks, sq.tail_tokens
+    vc, vm, vs, vsum, vcount = sq.v_codes, sq.v_min, sq.v_scale, sq.v_sum, sq.v_count
+    if T == 0:                                   # the token opens a new block
+        vc = np.concatenate([vc, np.zeros((1, Pi, d), np.int64)])
+        vm = np.concatenate([vm, np.zeros((1, d))]); vs = np.concatenate([vs, np.zeros((1, d))])
+        vsum = np.concatenate([vsum, np.zeros((1, d), np.int64)]); vcount = np.concatenate([vcount, [0]])
+        vals = v_row[None, :]
+    else:
+        old = dequantize_to_f16(vc[F, :T, :], vm[F][None, :], vs[F][None, :])   # [T][d]
+        vals = np.concatenate([old, v_row[None, :]])
+    uv = None
+    if rounding == STOCHASTIC:
+        toks = F * Pi + np.arange(T + 1)
+        uv = stochastic_threshold(seed, STREAM_V, element_index(seq, kv_heads, head, toks[None, :], np.arange(d)[:, None], d))
+    c, m, s_, tot = quantize_partition(vals.T, bits, "f16", rounding, uv)          # [d][T+1]
+    vc = vc.copy(); vm = vm.copy(); vs = vs.copy(); vsum = vsum.copy(); vcount = vcount.copy()
+    vc[F, :, :] = 0
+    vc[F, :T + 1, :] = c.T
+    vm[F] = m; vs[F] = s_; vsum[F] = tot; vcount[F] = T + 1
+    tail = np.concatenate([sq.v_tail, v_row[None, :]]) if T + 1 < Pi else np.zeros((0, d), np.float16)
+    return SeqKV(L + 1, Pi, np.concatenate([sq.k_codes, kc.reshape(1, d)]),
+                 np.concatenate([sq.k_min, km.astype(np.float64)[None, :]]),
+                 np.concatenate([sq.k_scale, ks.astype(np.float64)[None, :]]),
+                 np.concatenate([sq.k_sum, ksum[None, :]]), vc, vm, vs, vsum, vcount, tail)
 
 
 def dequantize_k(sq: SeqKV) -> np.ndarray:

@@ -181,3 +181,60 @@ def test_planted_mistakes_are_caught(monkeypatch):
     xr = _rand_f16(8, (2000, 32))
     c, m, s, _ = _round_to_nearest_scale(xr, 2)
     assert c.max() > 3 or np.any(s < (xr.max(1).astype(np.float64) - xr.min(1)) / 3)   # range pin fails
+
+
+# ---- the requantizing open block (the alternative to requantization elimination, R15) ----
+def test_requantizing_append_reproduces_the_worked_example():
+    """Sec. 5.3's figure: the open block holds -2.1 and 1.7 (codes 0, 3); appending -2.9
+    (below the old minimum) through dequantize -> add -> quantize gives the hand-derived
+    block of tests/golden (codes 1, 3, 0 with the new min and the fp16-rounded-up scale)."""
+    ex = json.load(open(os.path.join(GOLDEN, "v_last_group.json")))
+    v = np.zeros((2, 32), np.float16)
+    v[:, 0] = np.array(ex["old_block"]["values"], np.float16)
+    sq = O.quantize_sequence(np.zeros((2, 32), np.float16), v, ex["bits"], 32)
+    assert list(sq.v_codes[0, :2, 0]) == ex["old_block"]["codes"]
+    new = np.zeros(32, np.float16)
+    new[0] = ex["new_block"]["values"][2]
+    sq2 = O.append_requantizing(sq, np.zeros(32, np.float16), new, ex["bits"])
+    assert list(sq2.v_codes[0, :3, 0]) == ex["new_block"]["codes"]
+    assert float(sq2.v_min[0, 0]) == ex["new_block"]["min"]
+    assert float(sq2.v_scale[0, 0]) == ex["new_block"]["scale"]
+    assert sq2.v_sum[0, 0] == sum(ex["new_block"]["codes"]) and sq2.v_count[0] == 3
+
+
+def test_requantizing_append_matches_fresh_quantization_where_nothing_was_requantized():
+    """K rows never depend on the open block; a token that opens a new block (n = 1) and
+    a block closed from a fresh start agree with quantizing the longer sequence."""
+    k = _rand_f16(3, (70, 128))
+    v = _rand_f16(4, (70, 128))
+    sq = O.quantize_sequence(k[:64], v[:64], 2, 32)
+    sq = O.append_requantizing(sq, k[64], v[64], 2)           # opens block 2 with one token
+    ref = O.quantize_sequence(k[:65], v[:65], 2, 32)
+    for f in ("k_codes", "k_min", "k_scale", "k_sum", "v_codes", "v_min", "v_scale", "v_sum", "v_count"):
+        assert np.array_equal(getattr(sq, f), getattr(ref, f)), f
+    for t in range(65, 70):
+        sq = O.append_requantizing(sq, k[t], v[t], 2)
+    ref = O.quantize_sequence(k[:70], v[:70], 2, 32)
+    assert np.array_equal(sq.k_codes, ref.k_codes) and np.array_equal(sq.k_scale, ref.k_scale)
+    assert np.array_equal(sq.v_codes[:2], ref.v_codes[:2])      # closed blocks untouched
+
+
+def test_requantizing_error_accumulates_within_its_bound():
+    """Building a block by 32 requantizing appends keeps every earlier rounding error:
+    each element's error |x - x_hat| stays within the sum of s/2 over the quantizations it
+    went through, and on average exceeds the error of quantizing the originals once."""
+    bits, Pi, d = 2, 32, 128
+    k = _rand_f16(5, (Pi, d))
+    v = _rand_f16(6, (Pi, d))
+    sq = O.quantize_sequence(k[:0], v[:0], bits, Pi)
+    bound = np.zeros((Pi, d))
+    for t in range(Pi):
+        sq = O.append_requantizing(sq, k[t], v[t], bits)
+        bound[:t + 1] += sq.v_scale[0][None, :] * (0.5 + 2.0 ** -14)
+    vhat = sq.v_codes[0] * sq.v_scale[0][None, :] + sq.v_min[0][None, :]
+    err = np.abs(vhat - v.astype(np.float64))
+    # every step also rounds the dequantized values to fp16 (half an ulp of |x| <= 2^-11 |x|)
+    assert np.all(err <= bound + Pi * 2.0 ** -11 * (np.abs(v.astype(np.float64)) + 8.0))
+    once = O.quantize_sequence(k, v, bits, Pi)
+    err_once = np.abs(once.v_codes[0] * once.v_scale[0][None, :] + once.v_min[0][None, :] - v.astype(np.float64))
+    assert err.mean() > err_once.mean()
