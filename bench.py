@@ -452,7 +452,7 @@ def bench_workload(name: str, steps: int, warmup: int):
     knew = [k_all[:, :, L0 + i].contiguous() for i in range(nsteps)]
     vnew = [v_all[:, :, L0 + i].contiguous() for i in range(nsteps)]
     for bits in (2, 4):
-        for tail in (hk.TAIL_FP16, hk.TAIL_REQUANT):
+        for tail in (hk.TAIL_FP16, hk.TAIL_REQUANT, hk.TAIL_DEQUANT):
             lay = hk.hack_kv_layout_make(d, H, bits, pi, cap)
             cache = hk.KVCache(lay, B, B, None, dev)
             lens = torch.full((B,), L0, dtype=torch.int32, device=dev)
@@ -477,7 +477,8 @@ def bench_workload(name: str, steps: int, warmup: int):
             dbytes = np.mean([B * H * decode_bytes_per_seq_head(L0 + i + 1, d, bits, pi, sb) for i in range(nsteps)])
             dbytes += B * Hq * d * 6
             abytes = np.mean([append_bytes(B, H, d, bits, pi, sb, (L0 + i + 1) % pi) for i in range(nsteps)])
-            print(json.dumps({"workload": name, "kv_bits": bits, "tail_mode": "requant" if tail else "fp16",
+            print(json.dumps({"workload": name, "kv_bits": bits,
+                              "tail_mode": {0: "fp16", 1: "requant", 2: "dequant_requant"}[tail],
                               "metric": "append+decode GB/s", "value": round((dbytes + abytes) / step_ms / 1e6, 2),
                               "unit": "GB/s", "ms_per_step": round(step_ms, 4), "decode_bytes": int(dbytes),
                               "frac_of_8TBs": round((dbytes + abytes) / step_ms / 1e6 / HBM_PEAK_GBS, 4)}),

@@ -55,7 +55,12 @@ enum { HACK_ROUND_NEAREST_EVEN = 0, HACK_ROUND_STOCHASTIC = 1 };
  * FP16    - kept in fp16 and multiplied with the unquantized P (the paper's default);
  * REQUANT - re-quantized from its fp16 originals with n = T on every append, and
  *           multiplied through Eq. 4 with n = T. */
-enum { HACK_TAIL_FP16 = 0, HACK_TAIL_REQUANT = 1 };
+/* Open V block modes (Sec. 5.3): FP16 keeps it in fp16 (requantization elimination,
+ * the paper's default); REQUANT re-quantizes it from its fp16 values on every append;
+ * DEQUANT re-quantizes it from its dequantized codes plus the new value on every
+ * append (the alternative the paper's requantization elimination replaces, whose
+ * rounding errors accumulate).  REQUANT and DEQUANT attend over the block's codes. */
+enum { HACK_TAIL_FP16 = 0, HACK_TAIL_REQUANT = 1, HACK_TAIL_DEQUANT = 2 };
 
 /* Device arrays of a quantized KV cache.  Let P = head_dim/partition,
  * CB = head_dim*kv_bits/8 (code bytes per token), VB = partition*kv_bits/8 (code
@@ -149,7 +154,9 @@ hack_status hack_quantize(const hack_kv_layout* layout, const hack_kv_cache* cac
  * seq_lens[s]: its K partitions are quantized (earlier K partitions never change);
  * its V values enter the fp16 open block; when the open block reaches Pi tokens it is
  * quantized as a full block.  In HACK_TAIL_REQUANT mode the open block is also
- * re-quantized from its fp16 values on every call (n = T).  A cache must be
+ * re-quantized from its fp16 values on every call (n = T); in HACK_TAIL_DEQUANT mode
+ * its codes are dequantized to fp16, x = fp16(fl(fl(s*code) + min)), the new value is
+ * added and the block is quantized again (also when it fills).  A cache must be
  * attended with the tail mode it was appended with.  seq_lens_dev is incremented on
  * the device.  max_len is a host upper bound of seq_lens before the call; returns
  * HACK_ERR_CAPACITY if max_len + 1 exceeds the capacity (the kernel also skips any

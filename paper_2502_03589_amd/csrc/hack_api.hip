@@ -139,7 +139,7 @@ hack_status hack_append(const hack_kv_layout* layout, const hack_kv_cache* cache
                         int32_t tail_mode, hipStream_t stream) {
   if (!layout_ok(layout) || !k_new_dev || !v_new_dev || !seq_lens_dev || batch < 0 || max_len < 0)
     return HACK_ERR_INVALID_ARGUMENT;
-  if (!(tail_mode == HACK_TAIL_FP16 || tail_mode == HACK_TAIL_REQUANT)) return HACK_ERR_INVALID_ARGUMENT;
+  if (!(tail_mode == HACK_TAIL_FP16 || tail_mode == HACK_TAIL_REQUANT || tail_mode == HACK_TAIL_DEQUANT)) return HACK_ERR_INVALID_ARGUMENT;
   const int64_t cap = cache_capacity(layout, cache, batch);
   if (cap < 0) return HACK_ERR_INVALID_ARGUMENT;
   if ((int64_t)max_len + 1 > cap) return HACK_ERR_CAPACITY;
@@ -148,7 +148,7 @@ hack_status hack_append(const hack_kv_layout* layout, const hack_kv_cache* cache
   (void)hipGetLastError();
   return from_hip(hack::launch_append(*layout, make_view(layout, cache), static_cast<const __half*>(k_new_dev),
                                       static_cast<const __half*>(v_new_dev), seq_lens_dev, batch, (int)cap,
-                                      tail_mode == HACK_TAIL_REQUANT, stream));
+                                      tail_mode, stream));
 }
 
 int64_t hack_decode_workspace_bytes(const hack_kv_layout* layout, int32_t batch, int32_t num_q_heads,
@@ -198,7 +198,7 @@ hack_status hack_attend_decode(const hack_kv_layout* layout, const hack_kv_cache
   int64_t cap = 0;
   hack_status st = decode_common(layout, cache, q_dev, num_q_heads, seq_lens_dev, batch, max_len, a, &cap);
   if (st != HACK_OK) return st;
-  if (!out_dev || !(tail_mode == HACK_TAIL_FP16 || tail_mode == HACK_TAIL_REQUANT))
+  if (!out_dev || !(tail_mode == HACK_TAIL_FP16 || tail_mode == HACK_TAIL_REQUANT || tail_mode == HACK_TAIL_DEQUANT))
     return HACK_ERR_INVALID_ARGUMENT;
   const hack::DecodePlan plan = hack::plan_decode(*layout, batch, num_q_heads, max_len);
   if (!workspace_dev || workspace_bytes < plan.workspace_bytes) return HACK_ERR_WORKSPACE;
@@ -208,7 +208,7 @@ hack_status hack_attend_decode(const hack_kv_layout* layout, const hack_kv_cache
   a.counters = reinterpret_cast<int32_t*>(static_cast<uint8_t*>(workspace_dev) + plan.counter_offset);
   a.chunk = plan.chunk;
   a.splits = plan.splits;
-  a.tail_requant = tail_mode == HACK_TAIL_REQUANT;
+  a.tail_requant = tail_mode;  // 0: fp16 open block; 1, 2: its codes (re-quantized on append)
   (void)hipGetLastError();
   return from_hip(hack::launch_decode(*layout, a, batch, hack::MODE_ATTEND, stream));
 }
@@ -225,7 +225,7 @@ hack_status hack_decode_step(const hack_kv_layout* layout, const hack_kv_cache* 
   hack_status st = decode_common(layout, cache, q_dev, num_q_heads, seq_lens_in_dev, batch, max_len + 1, a, &cap);
   if (st != HACK_OK) return st;
   if (!k_new_dev || !v_new_dev || !seq_lens_out_dev || !out_dev || seq_lens_out_dev == seq_lens_in_dev ||
-      !(tail_mode == HACK_TAIL_FP16 || tail_mode == HACK_TAIL_REQUANT))
+      !(tail_mode == HACK_TAIL_FP16 || tail_mode == HACK_TAIL_REQUANT || tail_mode == HACK_TAIL_DEQUANT))
     return HACK_ERR_INVALID_ARGUMENT;
   const hack::DecodePlan plan = hack::plan_decode(*layout, batch, num_q_heads, max_len + 1);
   if (!workspace_dev || workspace_bytes < plan.workspace_bytes) return HACK_ERR_WORKSPACE;
@@ -235,7 +235,7 @@ hack_status hack_decode_step(const hack_kv_layout* layout, const hack_kv_cache* 
   a.counters = reinterpret_cast<int32_t*>(static_cast<uint8_t*>(workspace_dev) + plan.counter_offset);
   a.chunk = plan.chunk;
   a.splits = plan.splits;
-  a.tail_requant = tail_mode == HACK_TAIL_REQUANT;
+  a.tail_requant = tail_mode;  // 0: fp16 open block; 1, 2: its codes (re-quantized on append)
   a.k_new = static_cast<const __half*>(k_new_dev);
   a.v_new = static_cast<const __half*>(v_new_dev);
   a.lens_out = seq_lens_out_dev;

@@ -174,16 +174,67 @@ __device__ __forceinline__ void store_codes(uint8_t* dst, const uint32_t (&w)[(P
   for (int i = 0; i < (PI * BITS + 31) / 32; ++i) d[i] = w[i];
 }
 
+// Open V block modes (the library's HACK_TAIL_* values).
+constexpr int kTailFp16 = 0, kTailRequant = 1, kTailDequant = 2;
+
+// The new token's V value of channel `ch` (Sec. 5.3): it goes to row T = L mod PI of
+// the fp16 open block, and the block (n = T + 1 values) is quantized when it fills or,
+// in the re-quantizing modes, on every append.  Requant takes the earlier values from
+// the fp16 rows; Dequant recovers them from the block's codes,
+// x = fp16(fl(fl(s * code) + min)), so every earlier rounding error is kept.
+template <int BITS, int PI>
+__device__ __forceinline__ void append_v_channel(const CacheView& c, int s, int h, int L, int ch, __half vn,
+                                                 int tail_mode, bool stochastic, uint64_t key_v) {
+  const int H = c.kv_heads, d = c.head_dim;
+  const int F = L / PI, T = L - F * PI;  // the new token is element T of block F
+  __half* tail = c.v_tail + (((int64_t)s * H + h) * PI) * d + ch;  // row 0 of the open block
+  tail[(int64_t)T * d] = vn;
+  if (!(T + 1 == PI || tail_mode != kTailFp16)) return;
+  constexpr int NW = (PI * BITS + 31) / 32;
+  const int64_t vbh = v_block<PI>(c, s, h, F * PI);
+  uint32_t* cdst = reinterpret_cast<uint32_t*>(c.v_codes + (vbh * d + ch) * (PI * BITS / 8));
+  float x[PI];
+  if (tail_mode == kTailDequant) {
+    uint32_t old[NW];
+#pragma unroll
+    for (int w = 0; w < NW; ++w) old[w] = T > 0 ? cdst[w] : 0u;
+    const uint32_t meta = T > 0 ? reinterpret_cast<const uint32_t*>(c.v_meta)[vbh * d + ch] : 0u;
+    const float mn = __half2float(__ushort_as_half((uint16_t)(meta & 0xFFFFu)));
+    const float sc = __half2float(__ushort_as_half((uint16_t)(meta >> 16)));
+#pragma unroll
+    for (int e = 0; e < PI; ++e) {
+      const float code = (float)((old[(e * BITS) / 32] >> ((e * BITS) % 32)) & ((1u << BITS) - 1u));
+      const float xe = __half2float(__float2half_rn(__fadd_rn(__fmul_rn(sc, code), mn)));
+      x[e] = e < T ? xe : (e == T ? __half2float(vn) : 0.0f);
+    }
+  } else {
+    // every row of the open block is read (rows past T are ignored), so the loads
+    // are independent of T and issue together
+    __half raw[PI];
+#pragma unroll
+    for (int e = 0; e < PI; ++e) raw[e] = tail[(int64_t)e * d];
+#pragma unroll
+    for (int e = 0; e < PI; ++e) x[e] = e < T ? __half2float(raw[e]) : (e == T ? __half2float(vn) : 0.0f);
+  }
+  uint32_t words[NW];
+  uint16_t mb, sb;
+  const uint32_t sum = quantize_values<BITS, PI>(x, T + 1, stochastic, key_v, element_index(s, H, h, F * PI, d, ch),
+                                                 (uint64_t)d, words, mb, sb);
+#pragma unroll
+  for (int w = 0; w < NW; ++w) cdst[w] = words[w];
+  reinterpret_cast<uint32_t*>(c.v_meta)[vbh * d + ch] = (uint32_t)mb | ((uint32_t)sb << 16);
+  store_sum(c.v_sums, vbh * d + ch, c.sum_bytes, sum);
+}
+
 // Quantize-on-write of one token of one (sequence, kv head) (Sec. 5.3): the new
 // token is token L of the sequence.  Its K row is quantized per partition; its V
-// values go to row T = L mod PI of the fp16 open block, and the block is quantized
-// (n = T + 1 values per channel) when it fills or when `requant` is set.  Threads
-// tid < d/PI take one K partition each, threads tid, tid + nthreads, ... one V
-// channel each.  The caller guarantees 0 <= L < capacity.
+// values go through append_v_channel.  Threads tid < d/PI take one K partition each,
+// threads tid, tid + nthreads, ... one V channel each.  The caller guarantees
+// 0 <= L < capacity.
 template <int BITS, int PI>
 __device__ __forceinline__ void append_head(const CacheView& c, const __half* __restrict__ k_new,
                                             const __half* __restrict__ v_new, int s, int h, int L,
-                                            bool requant, bool stochastic, uint64_t key_k, uint64_t key_v,
+                                            int tail_mode, bool stochastic, uint64_t key_k, uint64_t key_v,
                                             int tid, int nthreads) {
   const int H = c.kv_heads, d = c.head_dim, P = d / PI;
   if (tid < P) {
@@ -198,31 +249,8 @@ __device__ __forceinline__ void append_head(const CacheView& c, const __half* __
     reinterpret_cast<uint32_t*>(c.k_meta)[row * P + tid] = (uint32_t)mb | ((uint32_t)sb << 16);
     store_sum(c.k_sums, row * P + tid, c.sum_bytes, sum);
   }
-  const int F = L / PI, T = L - F * PI;  // the new token is element T of block F
-  const bool quantize_v = T + 1 == PI || requant;
-  for (int ch = tid; ch < d; ch += nthreads) {
-    const __half vn = v_new[ch];
-    __half* tail = c.v_tail + (((int64_t)s * H + h) * PI) * d + ch;
-    tail[(int64_t)T * d] = vn;
-    if (quantize_v) {
-      // every row of the open block is read (rows past T are ignored), so the loads
-      // are independent of T and issue together
-      __half raw[PI];
-#pragma unroll
-      for (int e = 0; e < PI; ++e) raw[e] = tail[(int64_t)e * d];
-      float x[PI];
-#pragma unroll
-      for (int e = 0; e < PI; ++e) x[e] = e < T ? __half2float(raw[e]) : (e == T ? __half2float(vn) : 0.0f);
-      uint32_t words[(PI * BITS + 31) / 32];
-      uint16_t mb, sb;
-      const uint32_t sum = quantize_values<BITS, PI>(x, T + 1, stochastic, key_v,
-                                                     element_index(s, H, h, F * PI, d, ch), (uint64_t)d, words, mb, sb);
-      const int64_t vbh = v_block<PI>(c, s, h, F * PI);
-      store_codes<BITS, PI>(c.v_codes + (vbh * d + ch) * (PI * BITS / 8), words);
-      reinterpret_cast<uint32_t*>(c.v_meta)[vbh * d + ch] = (uint32_t)mb | ((uint32_t)sb << 16);
-      store_sum(c.v_sums, vbh * d + ch, c.sum_bytes, sum);
-    }
-  }
+  for (int ch = tid; ch < d; ch += nthreads)
+    append_v_channel<BITS, PI>(c, s, h, L, ch, v_new[ch], tail_mode, stochastic, key_v);
 }
 
 // ---------------------------------------------------------------------------

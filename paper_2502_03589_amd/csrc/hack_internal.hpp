@@ -29,7 +29,7 @@ hipError_t launch_quantize(const hack_kv_layout& lay, const CacheView& c, const 
 
 hipError_t launch_append(const hack_kv_layout& lay, const CacheView& c, const __half* k_new,
                          const __half* v_new, int32_t* lens, int batch, int capacity,
-                         int tail_requant, hipStream_t stream);
+                         int tail_mode, hipStream_t stream);
 
 enum DecodeMode { MODE_ATTEND = 0, MODE_QK = 1, MODE_PV = 2 };
 
@@ -45,7 +45,7 @@ struct DecodeArgs {
   int head_groups;        // workgroups per (sequence, kv head, chunk), each for up to 4*GT heads
   int chunk;
   int splits;
-  int tail_requant;
+  int tail_requant;       // open V block mode: 0 fp16, 1 / 2 its codes (re-quantized from fp16 / from codes)
   int max_len;
   float qmax;             // 2^b_QP - 1 of the transient Q and P codes (15 or 255)
   float inv_qmax;         // 1 / qmax

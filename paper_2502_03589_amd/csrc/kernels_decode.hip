@@ -410,7 +410,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
     if (split == 0 && blockIdx.x == 0 && tid == 0) a.lens_out[s] = Lq;
     if (ok && Lin / a.chunk == split) {
       append_head<BITS, PI>(c, a.k_new + ((int64_t)s * H + hkv) * D, a.v_new + ((int64_t)s * H + hkv) * D, s, hkv,
-                            Lin, a.tail_requant != 0, a.stochastic != 0, a.key_k, a.key_v, tid, 256);
+                            Lin, a.tail_requant, a.stochastic != 0, a.key_k, a.key_v, tid, 256);
       __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): the appended bytes are in L2
       __syncthreads();
     }

@@ -113,13 +113,14 @@ __global__ __launch_bounds__(256) void quantize_v_kernel(CacheView c, const __ha
 }
 
 // One new token per sequence: K partitions of the token; V value into the fp16
-// open block, which is quantized when it fills (and on every call in REQUANT mode).
+// open block, which is quantized when it fills (and on every call in the
+// re-quantizing modes, see append_v_channel).
 // The new token's values are loaded together with the sequence length (they do not
 // depend on it) so that the kernel pays one memory round trip before its stores.
 template <int BITS, int PI>
 __global__ __launch_bounds__(256) void append_kernel(CacheView c, const __half* __restrict__ k_new,
                                                      const __half* __restrict__ v_new, int32_t* lens,
-                                                     int capacity, int requant, int stochastic,
+                                                     int capacity, int tail_mode, int stochastic,
                                                      uint64_t key_k, uint64_t key_v) {
   constexpr int MAXV = 8;  // V channels per thread: H * d <= 256 * MAXV
   const int s = blockIdx.x;
@@ -151,33 +152,11 @@ __global__ __launch_bounds__(256) void append_kernel(CacheView c, const __half* 
     reinterpret_cast<uint32_t*>(c.k_meta)[row * P + p] = (uint32_t)mb | ((uint32_t)sb << 16);
     store_sum(c.k_sums, row * P + p, c.sum_bytes, sum);
   }
-  const int F = L / PI, T = L - F * PI;  // the new token is element T of block F
-  const bool quantize_v = T + 1 == PI || requant;
 #pragma unroll
   for (int i = 0; i < MAXV; ++i) {
     const int w = threadIdx.x + i * blockDim.x;
     if (w >= nv) break;
-    const int h = w / d, ch = w % d;
-    __half* tail = c.v_tail + (((int64_t)s * H + h) * PI) * d + ch;
-    tail[(int64_t)T * d] = vn[i];
-    if (quantize_v) {
-      const int n = T + 1;
-      // every row of the open block is read (rows past T are ignored): independent loads
-      __half raw[PI];
-#pragma unroll
-      for (int e = 0; e < PI; ++e) raw[e] = tail[(int64_t)e * d];
-      float x[PI];
-#pragma unroll
-      for (int e = 0; e < PI; ++e) x[e] = e < T ? __half2float(raw[e]) : (e == T ? __half2float(vn[i]) : 0.0f);
-      uint32_t words[(PI * BITS + 31) / 32];
-      uint16_t mb, sb;
-      const uint32_t sum = quantize_values<BITS, PI>(
-          x, n, stochastic != 0, key_v, element_index(s, H, h, F * PI, d, ch), (uint64_t)d, words, mb, sb);
-      const int64_t vbh = v_block<PI>(c, s, h, F * PI);
-      store_codes<BITS, PI>(c.v_codes + (vbh * d + ch) * (PI * BITS / 8), words);
-      reinterpret_cast<uint32_t*>(c.v_meta)[vbh * d + ch] = (uint32_t)mb | ((uint32_t)sb << 16);
-      store_sum(c.v_sums, vbh * d + ch, c.sum_bytes, sum);
-    }
+    append_v_channel<BITS, PI>(c, s, w / d, L, w % d, vn[i], tail_mode, stochastic != 0, key_v);
   }
   __syncthreads();  // every thread has read lens[s]
   if (threadIdx.x == 0) lens[s] = L + 1;
@@ -204,10 +183,10 @@ static hipError_t quantize_impl(const hack_kv_layout& lay, const CacheView& c, c
 template <int BITS, int PI>
 static hipError_t append_impl(const hack_kv_layout& lay, const CacheView& c, const __half* k_new,
                               const __half* v_new, int32_t* lens, int batch, int capacity,
-                              int tail_requant, hipStream_t stream) {
+                              int tail_mode, hipStream_t stream) {
   const int stoch = lay.rounding == HACK_ROUND_STOCHASTIC;
   hipLaunchKernelGGL((append_kernel<BITS, PI>), dim3(batch), dim3(256), 0, stream, c, k_new, v_new, lens,
-                     capacity, tail_requant, stoch, stream_key(lay.seed, 1), stream_key(lay.seed, 2));
+                     capacity, tail_mode, stoch, stream_key(lay.seed, 1), stream_key(lay.seed, 2));
   return hipGetLastError();
 }
 
@@ -234,8 +213,8 @@ hipError_t launch_quantize(const hack_kv_layout& lay, const CacheView& c, const 
 
 hipError_t launch_append(const hack_kv_layout& lay, const CacheView& c, const __half* k_new,
                          const __half* v_new, int32_t* lens, int batch, int capacity,
-                         int tail_requant, hipStream_t stream) {
-#define CALLA(B, P) append_impl<B, P>(lay, c, k_new, v_new, lens, batch, capacity, tail_requant, stream)
+                         int tail_mode, hipStream_t stream) {
+#define CALLA(B, P) append_impl<B, P>(lay, c, k_new, v_new, lens, batch, capacity, tail_mode, stream)
   HACK_DISPATCH_BITS_PI(lay.kv_bits, lay.partition, CALLA)
 #undef CALLA
 }

@@ -22,6 +22,7 @@ ROUND_NEAREST_EVEN = 0
 ROUND_STOCHASTIC = 1
 TAIL_FP16 = 0
 TAIL_REQUANT = 1
+TAIL_DEQUANT = 2
 K_CODES, K_META, K_SUMS, V_CODES, V_META, V_SUMS, V_TAIL = range(7)
 SECTIONS = ("k_codes", "k_meta", "k_sums", "v_codes", "v_meta", "v_sums", "v_tail")
 
