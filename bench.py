@@ -123,6 +123,8 @@ def copy_calibration(mib: int = 512, iters: int = 5):
 def cpu_baseline_decode(wl, budget_s: float = 15.0):
     """The oracle timed on host cores over a bounded sample of the decode workload:
     whole (sequence, kv head) pairs at the full context, all G query heads each."""
+    from threadpoolctl import threadpool_limits
+
     from oracle import hack_oracle as O
     from paper_2502_03589_amd import synth
     d, L, G = wl.head_dim, wl.context, wl.group
@@ -135,10 +137,11 @@ def cpu_baseline_decode(wl, budget_s: float = 15.0):
         v = synth.normal_f16(wl.seed, "v", (L, d), sub=1 + pairs)
         q = synth.normal_f16(wl.seed, "q", (G, d), sub=1 + pairs)
         sq = O.quantize_sequence(k, v, wl.kv_bits, wl.partition)
-        t0 = time.perf_counter()
-        for g in range(G):
-            O.decode_row(q[g], sq)
-        t_used += time.perf_counter() - t0
+        with threadpool_limits(1):  # numpy's BLAS on one thread, as reported in `cores`
+            t0 = time.perf_counter()
+            for g in range(G):
+                O.decode_row(q[g], sq)
+            t_used += time.perf_counter() - t0
         bytes_done += decode_bytes_per_seq_head(L, d, wl.kv_bits, wl.partition, sb) + G * d * (2 + 4)
         pairs += 1
     return {"value": round(bytes_done / t_used / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
