@@ -120,6 +120,25 @@ def copy_calibration(mib: int = 512, iters: int = 5):
     print(json.dumps({"copy_calibration_mib": mib, "launches": iters}), flush=True)
 
 
+def copy_bandwidth(mib: int = 1024, iters: int = 10) -> float:
+    """GB/s of a plain device-to-device copy (read + write bytes over the time): the
+    bandwidth a streaming kernel reaches on this machine, beside the 8 TB/s datasheet peak."""
+    import torch
+    src = torch.ones(mib << 18, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(iters):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / iters
+    del src, dst
+    return 2 * (mib << 20) / (ms * 1e-3) / 1e9
+
+
 def cpu_baseline_decode(wl, budget_s: float = 15.0):
     """The oracle timed on host cores over a bounded sample of the decode workload:
     whole (sequence, kv head) pairs at the full context, all G query heads each."""
@@ -271,6 +290,7 @@ def main():
                      "traffic": profiled_traffic("kernels_decode.hip", "decode_llama8b_l4096_hbm_counters.txt"),
                      "avg_kernel_us": round(avg_kern_ms * 1e3, 3),
                      "bytes_per_launch": int(step_bytes)},
+        "box_copy_GBs": round(copy_bandwidth(), 1),
         "quantize": {"workload": "decode_llama8b_l4096 prompt (hack_quantize of 16 x 8 x 4096 tokens)",
                      "ms": round(q_ms, 4), "GBs": round(q_gbs, 1), "frac_hbm": round(q_gbs / HBM_PEAK_GBS, 4)},
     }
