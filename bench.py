@@ -88,6 +88,27 @@ def profiled_traffic(kernel_file: str, summary: str):
         return None
 
 
+VALU_PEAK_LANE_OPS = 16 * 4 * 256 * 2.4e9  # 16 lanes x 4 SIMDs x 256 CUs x 2.4 GHz (unpacked fp32)
+
+
+def profiled_field(kernel_file: str, summary: str, field: str, sha_field: str = "kernel_source_sha256"):
+    """An integer field of a committed rocprofv3 summary, or None when the kernel source
+    has changed since the summary was taken."""
+    import hashlib
+    try:
+        text = open(os.path.join(ROOT, "profiles", summary)).read()
+        src = open(os.path.join(ROOT, "paper_2502_03589_amd", "csrc", kernel_file), "rb").read()
+    except OSError:
+        return None
+    fields = dict(line.split(": ", 1) for line in text.splitlines() if ": " in line and not line.startswith(" "))
+    if fields.get(sha_field, "").strip() != hashlib.sha256(src).hexdigest():
+        return None
+    try:
+        return int(fields[field])
+    except (KeyError, ValueError):
+        return None
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -344,10 +365,21 @@ def bench_prefill(iters: int, qp_bits: int = 8, rounding: int = 0):
     q_ms = float(np.median(qt))
     tops = ops / (a_ms * 1e-3) / 1e12
     q_gbs = quantize_bytes(B, H, L, d, wl.kv_bits, wl.partition, lay.sum_bytes) / (q_ms * 1e-3) / 1e9
-    return {"workload": "prefill_l8192", "qp_bits": qp_bits, "rounding": "stochastic" if rounding else "nearest",
-            "int8_ops": ops, "attend_ms": round(a_ms, 4),
-            "quantize_ms": round(q_ms, 4), "quantize_GBs": round(q_gbs, 1), "TOPS": round(tops, 2),
-            "peak_TOPS": INT8_PEAK_TOPS, "frac": round(tops / INT8_PEAK_TOPS, 4)}
+    res = {"workload": "prefill_l8192", "qp_bits": qp_bits, "rounding": "stochastic" if rounding else "nearest",
+           "int8_ops": ops, "attend_ms": round(a_ms, 4),
+           "quantize_ms": round(q_ms, 4), "quantize_GBs": round(q_gbs, 1), "TOPS": round(tops, 2),
+           "peak_TOPS": INT8_PEAK_TOPS, "frac": round(tops / INT8_PEAK_TOPS, 4)}
+    if qp_bits == 8 and rounding == 0:
+        # the path is bound by its VALU work: VALU lane-operations per second (profiled
+        # instruction count x 64 lanes over the measured time) against the VALU peak
+        n = profiled_field("kernels_prefill.hip", "prefill_l8192_valu_mfma_counters.txt", "prefill_valu_instructions_per_launch",
+                           "prefill_kernel_source_sha256")
+        if n is not None:
+            ach = n * 64 / (a_ms * 1e-3) / 1e12
+            res["alu_roofline"] = {"bound": "alu", "achieved": round(ach, 2), "peak": round(VALU_PEAK_LANE_OPS / 1e12, 1),
+                                   "unit": "T VALU lane-ops/s", "frac": round(ach * 1e12 / VALU_PEAK_LANE_OPS, 4),
+                                   "valu_instructions_per_launch": n}
+    return res
 
 
 def bench_workload(name: str, steps: int, warmup: int):
