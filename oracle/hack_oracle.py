@@ -369,6 +369,68 @@ def dequantize_v_blocks(sq: SeqKV) -> np.ndarray:
 
 
 # ----------------------------------------------------------------------------
+# Operation counts of Sec. 5.2 / 5.3 (one partition spanning the inner dimension)
+# ----------------------------------------------------------------------------
+def hq_matmul_cost(M: int, Z: int, N: int) -> tuple:
+    """(integer products, correction) of C = A B by Eq. 4 for A (M x Z), B (Z x N) as
+    one partition: 2MZN for sum a'b'; 2MN (s_a s_b times it), MN + MZ (m_b s_a sum a'),
+    MN + NZ (m_a s_b sum b'), 2MN (Z m_a m_b) and 3MN (adding the terms): 9MN + MZ + NZ."""
+    return 2 * M * Z * N, 9 * M * N + M * Z + N * Z
+
+
+def decode_approximation_cost(d: int, L: int, sums_cached: bool = True) -> int:
+    """Correction cost of one decode step (q K^T with M=1, Z=d, N=L; P V with M=1,
+    Z=L, N=d): 10(d + L) + 2dL; caching the K and V code sums (summation
+    elimination) removes the 2dL of their per-step recomputation."""
+    qk = hq_matmul_cost(1, d, L)[1]
+    pv = hq_matmul_cost(1, L, d)[1]
+    return qk + pv - (2 * d * L if sums_cached else 0)
+
+
+def dequantization_cost(d: int, L: int) -> int:
+    """Dequantizing K and V of one step, x = s c + m per element: 4dL."""
+    return 4 * d * L
+
+
+def count_eq4_ops(a_codes, m_a, s_a, b_codes, m_b, s_b) -> tuple:
+    """Eq. 4 for A (M x Z) and B (Z x N) as one partition, evaluated element by element
+    while counting every arithmetic operation.  Returns (C, integer ops, correction ops):
+    per row of A its code sum (Z additions) and s_a * sum a' (1 multiplication), per
+    column of B likewise, then per output element s_a s_b (A'B') (2), m_b (s_a sum a')
+    (1), m_a (s_b sum b') (1), Z m_a m_b (2) and three additions."""
+    A = np.asarray(a_codes, np.int64)
+    B = np.asarray(b_codes, np.int64)
+    M, Z = A.shape
+    N = B.shape[1]
+    iops = 0
+    fops = 0
+    u = []
+    for i in range(M):                      # s_a[i] * sum_z a'[i][z]
+        t = 0
+        for z in range(Z):
+            t += int(A[i, z]); fops += 1
+        u.append(float(s_a[i]) * t); fops += 1
+    v = []
+    for j in range(N):                      # s_b[j] * sum_z b'[z][j]
+        t = 0
+        for z in range(Z):
+            t += int(B[z, j]); fops += 1
+        v.append(float(s_b[j]) * t); fops += 1
+    C = np.zeros((M, N))
+    for i in range(M):
+        for j in range(N):
+            p = 0
+            for z in range(Z):
+                p += int(A[i, z]) * int(B[z, j]); iops += 2
+            t1 = float(s_a[i]) * float(s_b[j]) * p; fops += 2
+            t2 = float(m_b[j]) * u[i]; fops += 1
+            t3 = float(m_a[i]) * v[j]; fops += 1
+            t4 = Z * float(m_a[i]) * float(m_b[j]); fops += 2
+            C[i, j] = t1 + t2 + t3 + t4; fops += 3
+    return C, iops, fops
+
+
+# ----------------------------------------------------------------------------
 # Attention on quantized operands (Sec. 5.3 with Eq. 2-4)
 # ----------------------------------------------------------------------------
 def quantize_query(q, partition: int, bits: int = 8, sr: Optional[QPStochastic] = None):

@@ -363,3 +363,39 @@ def test_stochastic_p_blocks_are_unbiased():
     assert np.all(np.abs(outs.mean(axis=0) - exact) <= bound)
     assert not np.allclose(outs[0], outs[1])             # different seeds, different codes
     assert np.abs(near - exact).max() > 0                # nearest rounding is not the closed form
+
+
+# ---- operation counts of Sec. 5.2 / 5.3 ------------------------------------------
+def test_eq4_operation_count_matches_the_paper():
+    """Evaluating Eq. 4 element by element with an operation counter gives 2MZN integer
+    operations and 9MN + MZ + NZ correction operations (plus the M + N products of the
+    per-row and per-column factors, a lower-order term), and the same C as the
+    vectorised Eq. 4."""
+    g = np.random.default_rng(17)
+    for M, Z, N in ((1, 8, 5), (3, 16, 2), (4, 7, 6)):
+        A = g.integers(0, 4, size=(M, Z)); B = g.integers(0, 4, size=(Z, N))
+        ma, sa = g.normal(size=M), np.abs(g.normal(size=M)); mb, sb = g.normal(size=N), np.abs(g.normal(size=N))
+        C, iops, fops = O.count_eq4_ops(A, ma, sa, B, mb, sb)
+        int_cost, corr_cost = O.hq_matmul_cost(M, Z, N)
+        assert iops == int_cost == 2 * M * Z * N
+        assert fops == corr_cost + M + N
+        _, ref = O.hq_matmul(A, ma[:, None], sa[:, None], B, mb[None, :], sb[None, :], Z)
+        assert np.allclose(C, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_decode_cost_model_break_even_points():
+    """Sec. 5.3: per decode step the correction costs 10(d + L) + 2dL, and 10(d + L) once
+    the code sums are cached; dequantizing K and V costs 4dL.  With d = 128 the
+    dequantization exceeds the correction for L > 2.5 and exceeds it tenfold for L > 30
+    (exactly 31.07: the paper's 30 is approximate)."""
+    d = 128
+    assert O.decode_approximation_cost(d, 100, sums_cached=False) == 10 * (d + 100) + 2 * d * 100
+    assert O.decode_approximation_cost(d, 100) == 10 * (d + 100)
+    assert O.dequantization_cost(d, 2) < O.decode_approximation_cost(d, 2)
+    assert O.dequantization_cost(d, 3) > O.decode_approximation_cost(d, 3)
+    exact = 10 * d / (4 * d - 10)
+    assert 2.5 < exact < 2.6
+    ten = 100 * d / (4 * d - 100)
+    assert 31 < ten < 31.1
+    assert O.dequantization_cost(d, 31) < 10 * O.decode_approximation_cost(d, 31)
+    assert O.dequantization_cost(d, 32) > 10 * O.decode_approximation_cost(d, 32)
