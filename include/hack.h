@@ -182,8 +182,11 @@ int64_t hack_decode_workspace_bytes(const hack_kv_layout* layout, int32_t batch,
  * chunk records) and must not be shared by calls that may run concurrently.  One
  * kernel is launched; when a sequence is split into several chunks, the workgroup
  * that finishes its last chunk merges them.
- * Requires head_dim 128, partition 32 or 64, H_q/H_kv <= 8, batch <= 65535 and, for
- * a paged cache, page_tokens a multiple of 4 * partition (else HACK_ERR_UNSUPPORTED). */
+ * Requires head_dim 128, partition 32, 64 or 128, H_q/H_kv <= 8, batch <= 65535 and,
+ * for a paged cache, page_tokens a multiple of 4 * partition (else
+ * HACK_ERR_UNSUPPORTED).  Partitions of 32 and 64 run on the matrix cores; a
+ * partition of 128 (one K partition per token row, V blocks of 128 tokens) runs on
+ * the VALU's int8 dot instruction. */
 hack_status hack_attend_decode(const hack_kv_layout* layout, const hack_kv_cache* cache,
                                const void* q_dev, int32_t num_q_heads, const int32_t* seq_lens_dev,
                                int32_t batch, int32_t max_len, int32_t tail_mode, float* out_dev,
@@ -198,7 +201,9 @@ hack_status hack_attend_decode(const hack_kv_layout* layout, const hack_kv_cache
  * arrays must be distinct (callers swap them between steps).  max_len bounds
  * seq_lens_in; max_len + 1 must not exceed the capacity (HACK_ERR_CAPACITY).  The
  * workspace is the one hack_decode_workspace_bytes(layout, batch, H_q, max_len + 1)
- * sizes, zero-filled before first use as for hack_attend_decode. */
+ * sizes, zero-filled before first use as for hack_attend_decode.  With partition
+ * 128 the step is three operations on the stream (a copy of the lengths, the append
+ * kernel, the attention kernel), else one launch. */
 hack_status hack_decode_step(const hack_kv_layout* layout, const hack_kv_cache* cache,
                              const void* k_new_dev, const void* v_new_dev, const void* q_dev,
                              int32_t num_q_heads, const int32_t* seq_lens_in_dev,
@@ -211,8 +216,8 @@ hack_status hack_decode_step(const hack_kv_layout* layout, const hack_kv_cache* 
  * hack_quantize with all seq_lens = len.  q_dev: fp16 [batch][H_q][len][head_dim];
  * out_dev: fp32 [batch][H_q][len][head_dim].  causal != 0 masks token j > i for
  * query i; the masked zeros of P inside a block are quantized with the block.  The
- * open V block is used in fp16.  Requires head_dim 128, partition 32 or 64,
- * H_q % H_kv == 0, H_q/H_kv <= 8 and batch <= 65535 (else HACK_ERR_UNSUPPORTED). */
+ * open V block is used in fp16.  Requires head_dim 128, partition 32 or 64
+ * (128 is decode only), H_q % H_kv == 0, H_q/H_kv <= 8 and batch <= 65535 (else HACK_ERR_UNSUPPORTED). */
 hack_status hack_attend_prefill(const hack_kv_layout* layout, const hack_kv_cache* cache,
                                 const void* q_dev, int32_t num_q_heads, int32_t batch, int32_t len,
                                 int32_t causal, float* out_dev, hipStream_t stream);
@@ -220,7 +225,8 @@ hack_status hack_attend_prefill(const hack_kv_layout* layout, const hack_kv_cach
 /* Static, NUL-terminated description of a status code. */
 const char* hack_status_string(hack_status status);
 
-/* ---- test exports: integer products of the decode kernel, for bit-exact checks ---- */
+/* ---- test exports: integer products of the decode kernel, for bit-exact checks ----
+ * Partitions 32 and 64 only (HACK_ERR_UNSUPPORTED for 128). */
 
 /* Runs the decode kernel's QK^T stage only (Sec. 5.3, Eq. 4 integer part).
  * q_codes_dev: u8 [batch][H_q][head_dim] 8-bit Q codes; q_meta_dev: fp32

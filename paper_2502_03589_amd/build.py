@@ -14,7 +14,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OBJ = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libhack.so")
-SOURCES = ["hack_api.hip", "kernels_quant.hip", "kernels_decode.hip", "kernels_prefill.hip"]
+SOURCES = ["hack_api.hip", "kernels_quant.hip", "kernels_decode.hip", "kernels_decode128.hip",
+           "kernels_prefill.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

@@ -69,9 +69,15 @@ hack_status from_hip(hipError_t e) { return e == hipSuccess ? HACK_OK : HACK_ERR
 hack_status attention_shape(const hack_kv_layout* l, int num_q_heads) {
   if (num_q_heads < 1 || num_q_heads % l->num_kv_heads != 0) return HACK_ERR_INVALID_ARGUMENT;
   if (l->head_dim != 128) return HACK_ERR_UNSUPPORTED;
-  if (!(l->partition == 32 || l->partition == 64)) return HACK_ERR_UNSUPPORTED;
+  if (!(l->partition == 32 || l->partition == 64 || l->partition == 128)) return HACK_ERR_UNSUPPORTED;
   if (num_q_heads / l->num_kv_heads > 8) return HACK_ERR_UNSUPPORTED;
   return HACK_OK;
+}
+
+// Decode attention: partitions of 32 and 64 run the matrix-core kernel, 128 its own.
+hipError_t launch_attend(const hack_kv_layout& l, const hack::DecodeArgs& a, int batch, hipStream_t stream) {
+  if (l.partition == 128) return hack::launch_decode128(l, a, batch, stream);
+  return hack::launch_decode(l, a, batch, hack::MODE_ATTEND, stream);
 }
 
 }  // namespace
@@ -210,7 +216,7 @@ hack_status hack_attend_decode(const hack_kv_layout* layout, const hack_kv_cache
   a.splits = plan.splits;
   a.tail_requant = tail_mode;  // 0: fp16 open block; 1, 2: its codes (re-quantized on append)
   (void)hipGetLastError();
-  return from_hip(hack::launch_decode(*layout, a, batch, hack::MODE_ATTEND, stream));
+  return from_hip(launch_attend(*layout, a, batch, stream));
 }
 
 hack_status hack_decode_step(const hack_kv_layout* layout, const hack_kv_cache* cache, const void* k_new_dev,
@@ -244,7 +250,22 @@ hack_status hack_decode_step(const hack_kv_layout* layout, const hack_kv_cache* 
   a.key_k = layout->seed ^ (1ull << 56);
   a.key_v = layout->seed ^ (2ull << 56);
   (void)hipGetLastError();
-  return from_hip(hack::launch_decode(*layout, a, batch, hack::MODE_ATTEND, stream));
+  if (layout->partition == 128) {
+    // The partition-128 kernel attends only: the new lengths start as a copy of the
+    // old ones, the append kernel writes the token and bumps them, and the attention
+    // reads them (three operations on the stream instead of one launch).
+    if (layout->num_kv_heads * layout->head_dim > 2048) return HACK_ERR_UNSUPPORTED;  // one append workgroup
+    hipError_t e = hipMemcpyAsync(seq_lens_out_dev, seq_lens_in_dev, (size_t)batch * sizeof(int32_t),
+                                  hipMemcpyDeviceToDevice, stream);
+    if (e == hipSuccess)
+      e = hack::launch_append(*layout, a.c, a.k_new, a.v_new, seq_lens_out_dev, batch, (int)cap, tail_mode, stream);
+    if (e != hipSuccess) return from_hip(e);
+    a.lens = seq_lens_out_dev;
+    a.k_new = nullptr;
+    a.v_new = nullptr;
+    a.lens_out = nullptr;
+  }
+  return from_hip(launch_attend(*layout, a, batch, stream));
 }
 
 hack_status hack_attend_prefill(const hack_kv_layout* layout, const hack_kv_cache* cache, const void* q_dev,
@@ -254,6 +275,7 @@ hack_status hack_attend_prefill(const hack_kv_layout* layout, const hack_kv_cach
   const hack_status sh = attention_shape(layout, num_q_heads);
   if (sh != HACK_OK) return sh;
   if (layout->sum_bytes == 0) return HACK_ERR_UNSUPPORTED;  // prefill reads cached sums
+  if (layout->partition == 128) return HACK_ERR_UNSUPPORTED;  // decode only
   if (batch > kMaxGridYZ) return HACK_ERR_UNSUPPORTED;  // one grid plane per sequence
   const int64_t cap = cache_capacity(layout, cache, batch);
   if (cap < 0) return HACK_ERR_INVALID_ARGUMENT;
@@ -285,6 +307,7 @@ hack_status hack_debug_qk_products(const hack_kv_layout* layout, const hack_kv_c
   hack_status st = decode_common(layout, cache, q_dev, num_q_heads, seq_lens_dev, batch, max_len, a, &cap);
   if (st != HACK_OK) return st;
   if (layout->sum_bytes == 0) return HACK_ERR_UNSUPPORTED;  // the exports read cached sums
+  if (layout->partition == 128) return HACK_ERR_UNSUPPORTED;  // exports of the matrix-core kernel only
   if (!q_codes_dev || !q_meta_dev || !products_dev) return HACK_ERR_INVALID_ARGUMENT;
   if (batch == 0) return HACK_OK;
   const hack::DecodePlan plan = hack::plan_decode(*layout, batch, num_q_heads, max_len);
@@ -307,6 +330,7 @@ hack_status hack_debug_pv_products(const hack_kv_layout* layout, const hack_kv_c
   hack_status st = decode_common(layout, cache, p_codes_dev, num_q_heads, seq_lens_dev, batch, max_len, a, &cap);
   if (st != HACK_OK) return st;
   if (layout->sum_bytes == 0) return HACK_ERR_UNSUPPORTED;  // the exports read cached sums
+  if (layout->partition == 128) return HACK_ERR_UNSUPPORTED;  // exports of the matrix-core kernel only
   if (!p_meta_dev || !products_dev || !out_dev) return HACK_ERR_INVALID_ARGUMENT;
   if (batch == 0) return HACK_OK;
   const int span = 4 * layout->partition;

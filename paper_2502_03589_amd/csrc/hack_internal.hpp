@@ -72,6 +72,9 @@ struct DecodeArgs {
 hipError_t launch_decode(const hack_kv_layout& lay, const DecodeArgs& a, int batch, int mode,
                          hipStream_t stream);
 
+// Decode attention (MODE_ATTEND) for partition 128: VALU int8-dot kernel.
+hipError_t launch_decode128(const hack_kv_layout& lay, const DecodeArgs& a, int batch, hipStream_t stream);
+
 hipError_t launch_prefill(const hack_kv_layout& lay, const CacheView& c, const __half* q,
                           int num_q_heads, int batch, int len, int causal, float* out,
                           hipStream_t stream);
