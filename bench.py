@@ -413,7 +413,9 @@ def bench_workload(name: str, steps: int, warmup: int):
         R = 10
         for bits, part, se, rnd in ((2, 32, True, 0), (2, 64, True, 0), (4, 32, True, 0), (4, 64, True, 0),
                                     (2, 32, False, 0), (2, 64, False, 0), (4, 32, False, 0), (4, 64, False, 0),
-                                    (2, 32, True, 1), (4, 64, True, 1)):
+                                    (2, 32, True, 1), (4, 64, True, 1),
+                                    (2, 128, True, 0), (4, 128, True, 0), (2, 128, False, 0), (4, 128, False, 0),
+                                    (2, 128, True, 1)):
             # se=False: summation elimination off, no cached sums (fewer bytes, sums rebuilt);
             # rnd=1: stochastic rounding of K/V, Q and P codes
             lay = hk.hack_kv_layout_make(d, H, bits, part, L, 8, rnd, base.seed, sums_cached=se)

@@ -74,7 +74,13 @@ hack_status attention_shape(const hack_kv_layout* l, int num_q_heads) {
   return HACK_OK;
 }
 
-// Decode attention: partitions of 32 and 64 run the matrix-core kernel, 128 its own.
+// Decode attention: partitions of 32 and 64 run the matrix-core kernel, 128 its own
+// (with its own chunking of the sequences).
+hack::DecodePlan plan_attend(const hack_kv_layout& l, int batch, int num_q_heads, int max_len) {
+  return l.partition == 128 ? hack::plan_decode128(l, batch, num_q_heads, max_len)
+                            : hack::plan_decode(l, batch, num_q_heads, max_len);
+}
+
 hipError_t launch_attend(const hack_kv_layout& l, const hack::DecodeArgs& a, int batch, hipStream_t stream) {
   if (l.partition == 128) return hack::launch_decode128(l, a, batch, stream);
   return hack::launch_decode(l, a, batch, hack::MODE_ATTEND, stream);
@@ -162,7 +168,7 @@ int64_t hack_decode_workspace_bytes(const hack_kv_layout* layout, int32_t batch,
   if (!layout_ok(layout) || batch < 0 || max_len < 0 || num_q_heads < 1 ||
       num_q_heads % layout->num_kv_heads != 0)
     return -1;
-  return hack::plan_decode(*layout, batch, num_q_heads, max_len).workspace_bytes;
+  return plan_attend(*layout, batch, num_q_heads, max_len).workspace_bytes;
 }
 
 static hack_status decode_common(const hack_kv_layout* layout, const hack_kv_cache* cache, const void* q_dev,
@@ -206,7 +212,7 @@ hack_status hack_attend_decode(const hack_kv_layout* layout, const hack_kv_cache
   if (st != HACK_OK) return st;
   if (!out_dev || !(tail_mode == HACK_TAIL_FP16 || tail_mode == HACK_TAIL_REQUANT || tail_mode == HACK_TAIL_DEQUANT))
     return HACK_ERR_INVALID_ARGUMENT;
-  const hack::DecodePlan plan = hack::plan_decode(*layout, batch, num_q_heads, max_len);
+  const hack::DecodePlan plan = plan_attend(*layout, batch, num_q_heads, max_len);
   if (!workspace_dev || workspace_bytes < plan.workspace_bytes) return HACK_ERR_WORKSPACE;
   if (batch == 0) return HACK_OK;
   a.out = out_dev;
@@ -233,7 +239,7 @@ hack_status hack_decode_step(const hack_kv_layout* layout, const hack_kv_cache* 
   if (!k_new_dev || !v_new_dev || !seq_lens_out_dev || !out_dev || seq_lens_out_dev == seq_lens_in_dev ||
       !(tail_mode == HACK_TAIL_FP16 || tail_mode == HACK_TAIL_REQUANT || tail_mode == HACK_TAIL_DEQUANT))
     return HACK_ERR_INVALID_ARGUMENT;
-  const hack::DecodePlan plan = hack::plan_decode(*layout, batch, num_q_heads, max_len + 1);
+  const hack::DecodePlan plan = plan_attend(*layout, batch, num_q_heads, max_len + 1);
   if (!workspace_dev || workspace_bytes < plan.workspace_bytes) return HACK_ERR_WORKSPACE;
   if (batch == 0) return HACK_OK;
   a.out = out_dev;

@@ -22,6 +22,7 @@ struct DecodePlan {
 };
 
 DecodePlan plan_decode(const hack_kv_layout& lay, int batch, int num_q_heads, int max_len);
+DecodePlan plan_decode128(const hack_kv_layout& lay, int batch, int num_q_heads, int max_len);
 
 hipError_t launch_quantize(const hack_kv_layout& lay, const CacheView& c, const __half* k,
                            const __half* v, const int32_t* lens, int batch, int max_len,

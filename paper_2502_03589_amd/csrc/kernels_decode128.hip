@@ -14,6 +14,8 @@
 // sequence are merged by the workgroup that finishes last, from records written
 // with agent-coherent stores (the same protocol and workspace layout as the
 // partition-32/64 kernels).
+#include <algorithm>
+
 #include "hack_device.hpp"
 #include "hack_internal.hpp"
 
@@ -26,29 +28,34 @@ constexpr int kWaves128 = 4;  // waves per workgroup
 constexpr int kHeads = 4;     // query heads per workgroup
 constexpr float kLog2Scale = 0.12751743074941640f;  // log2(e) / sqrt(128): scores in log2 units
 constexpr float kRaiseSlack = 8.0f;                 // the reference max is raised lazily
+constexpr int kCUs = 256;                           // compute units of an MI355X
+
+// Workgroups per compute unit the register budget allows (the grid is sized for it).
+template <int BITS>
+constexpr int occupancy128() { return BITS == 2 ? 4 : 2; }
 
 __device__ __forceinline__ float f16_lo(uint32_t w) { return __half2float(__ushort_as_half((uint16_t)(w & 0xFFFFu))); }
 __device__ __forceinline__ float f16_hi(uint32_t w) { return __half2float(__ushort_as_half((uint16_t)(w >> 16))); }
 
+// Wave-wide reductions: a row of 16 lanes by DPP rotates, then the four row results
+// read into scalar registers (the result is wave-uniform).
+__device__ __forceinline__ float lane_f(float x, int l) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), l)); }
 __device__ __forceinline__ float wave_max(float x) {
-#pragma unroll
-  for (int m = 1; m < 64; m <<= 1) x = fmaxf(x, __shfl_xor(x, m, 64));
-  return x;
+  x = row16_max(x);
+  return fmaxf(fmaxf(lane_f(x, 0), lane_f(x, 16)), fmaxf(lane_f(x, 32), lane_f(x, 48)));
 }
 __device__ __forceinline__ float wave_min(float x) {
-#pragma unroll
-  for (int m = 1; m < 64; m <<= 1) x = fminf(x, __shfl_xor(x, m, 64));
-  return x;
+  x = row16_min(x);
+  return fminf(fminf(lane_f(x, 0), lane_f(x, 16)), fminf(lane_f(x, 32), lane_f(x, 48)));
 }
 __device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-  for (int m = 1; m < 64; m <<= 1) x += __shfl_xor(x, m, 64);
-  return x;
+  x = row16_sum(x);
+  return (lane_f(x, 0) + lane_f(x, 16)) + (lane_f(x, 32) + lane_f(x, 48));
 }
 __device__ __forceinline__ int wave_sum_i(int x) {
-#pragma unroll
-  for (int m = 1; m < 64; m <<= 1) x += __shfl_xor(x, m, 64);
-  return x;
+  x = row16_sum_i(x);
+  return (__builtin_amdgcn_readlane(x, 0) + __builtin_amdgcn_readlane(x, 16)) +
+         (__builtin_amdgcn_readlane(x, 32) + __builtin_amdgcn_readlane(x, 48));
 }
 
 // Byte position, inside a 128-byte operand, of element e (a channel of Q, a token
@@ -100,7 +107,8 @@ __device__ __forceinline__ void dot_rows(const uint32_t* x0, const uint32_t* x1,
   }
 }
 
-// sum of the codes packed in x[0..N), by population counts of the bit planes
+// sum of the codes packed in x[0..N): population counts of the bit planes (2-bit
+// codes) or the 4-bit dot instruction against ones (4-bit codes)
 template <int BITS, int N>
 __device__ __forceinline__ uint32_t sum_codes(const uint32_t* x) {
   uint32_t s = 0;
@@ -109,8 +117,7 @@ __device__ __forceinline__ uint32_t sum_codes(const uint32_t* x) {
     if constexpr (BITS == 2) {
       s += __popc(x[w] & 0x55555555u) + 2u * __popc(x[w] & 0xAAAAAAAAu);
     } else {
-      s += __popc(x[w] & 0x11111111u) + 2u * __popc(x[w] & 0x22222222u) + 4u * __popc(x[w] & 0x44444444u) +
-           8u * __popc(x[w] & 0x88888888u);
+      s = __builtin_amdgcn_udot8(x[w], 0x11111111u, s, false);  // eight 4-bit codes times one
     }
   }
   return s;
@@ -126,7 +133,7 @@ __device__ __forceinline__ void load_dwords(const uint8_t* p, uint32_t* x) {
 }
 
 template <int BITS, bool SE, bool SR>
-__global__ __launch_bounds__(256, 2) void decode128_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(256, occupancy128<BITS>()) void decode128_kernel(DecodeArgs a) {
   constexpr int KD = 4 * BITS;  // code dwords per K row, and per V channel of a block
   constexpr int REC = 4 + kD;   // chunk record: max, sum, 2 pad, O
 
@@ -426,24 +433,44 @@ __global__ __launch_bounds__(256, 2) void decode128_kernel(DecodeArgs a) {
   }
   __syncthreads();
   if (!last_chunk) return;
+  // one pass with a running max; the records of eight chunks are requested together
+  // so the merge waits on memory once per eight chunks
   for (int idx = tid; idx < Gl * (kD / 2); idx += 256) {
     const int gh = idx / (kD / 2), ch = 2 * (idx % (kD / 2));
-    float mrun = -INFINITY;
-    for (int sp = 0; sp < nsplit; ++sp) {
-      const float* rec = a.partials + ((pair * a.splits + sp) * G + head0 + gh) * REC;
-      const float l = __hip_atomic_load(rec + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (l > 0.0f) mrun = fmaxf(mrun, __hip_atomic_load(rec, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-    }
-    float lsum = 0.0f, x0 = 0.0f, x1 = 0.0f;
-    for (int sp = 0; sp < nsplit; ++sp) {
-      const float* rec = a.partials + ((pair * a.splits + sp) * G + head0 + gh) * REC;
-      const float l = __hip_atomic_load(rec + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (l > 0.0f) {
-        const float wt = __builtin_amdgcn_exp2f(__hip_atomic_load(rec, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) - mrun);
-        lsum = fmaf(l, wt, lsum);
-        x0 = fmaf(__hip_atomic_load(rec + 4 + ch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT), wt, x0);
-        x1 = fmaf(__hip_atomic_load(rec + 5 + ch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT), wt, x1);
+    float mrun = -INFINITY, lsum = 0.0f, x0 = 0.0f, x1 = 0.0f;
+    for (int sp0 = 0; sp0 < nsplit; sp0 += 8) {
+      float ms[8], ls[8], xa[8], xb[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        if (sp0 + u < nsplit) {
+          const float* rec = a.partials + ((pair * a.splits + sp0 + u) * G + head0 + gh) * REC;
+          ms[u] = __hip_atomic_load(rec, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          ls[u] = __hip_atomic_load(rec + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          xa[u] = __hip_atomic_load(rec + 4 + ch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          xb[u] = __hip_atomic_load(rec + 5 + ch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        } else {
+          ms[u] = -INFINITY;
+          ls[u] = 0.0f;
+          xa[u] = 0.0f;
+          xb[u] = 0.0f;
+        }
       }
+      float mn = mrun;
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (ls[u] > 0.0f) mn = fmaxf(mn, ms[u]);
+      const float wa = mrun == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(mrun - mn);
+      lsum *= wa;
+      x0 *= wa;
+      x1 *= wa;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const float wb = ls[u] > 0.0f ? __builtin_amdgcn_exp2f(ms[u] - mn) : 0.0f;
+        lsum = fmaf(ls[u], wb, lsum);
+        x0 = fmaf(xa[u], wb, x0);
+        x1 = fmaf(xb[u], wb, x1);
+      }
+      mrun = mn;
     }
     float* o = a.out + ((int64_t)s * Hq + hkv * G + head0 + gh) * kD + ch;
     const float inv = 1.0f / lsum;
@@ -469,6 +496,28 @@ hipError_t launch128_bits(const DecodeArgs& a, int batch, hipStream_t stream) {
 }
 
 }  // namespace
+
+// A chunk is a whole number of 4-block spans (one block per wave); chunks per
+// sequence are chosen so that the grid fills every compute unit at the kernel's
+// occupancy, at most 64 spans per chunk, and the grid's z extent stays <= 65535.
+DecodePlan plan_decode128(const hack_kv_layout& lay, int batch, int num_q_heads, int max_len) {
+  DecodePlan p{};
+  const int64_t span = (int64_t)kWaves128 * kBlk;
+  const int64_t pairs = (int64_t)batch * lay.num_kv_heads;
+  const int64_t G = lay.num_kv_heads > 0 ? num_q_heads / lay.num_kv_heads : 0;
+  const int64_t nhg = G > 0 ? (G + kHeads - 1) / kHeads : 1;
+  const int64_t target = (int64_t)kCUs * (lay.kv_bits == 2 ? occupancy128<2>() : occupancy128<4>());
+  const int64_t spans_seq = ((int64_t)max_len + span - 1) / span;
+  int64_t wg_spans = pairs > 0 ? (spans_seq * pairs * nhg + target - 1) / target : 1;
+  wg_spans = std::min<int64_t>(std::max<int64_t>(wg_spans, 1), 64);
+  wg_spans = std::max<int64_t>(wg_spans, (spans_seq + 65534) / 65535);
+  p.chunk = (int)(wg_spans * span);
+  p.splits = max_len > 0 ? (int)(((int64_t)max_len + p.chunk - 1) / p.chunk) : 1;
+  p.partial_floats = pairs * p.splits * G * (4 + kD);
+  p.counter_offset = ((p.partial_floats * 4 + 255) / 256) * 256;
+  p.workspace_bytes = p.counter_offset + ((pairs * nhg * 4 + 255) / 256) * 256;
+  return p;
+}
 
 hipError_t launch_decode128(const hack_kv_layout& lay, const DecodeArgs& args, int batch, hipStream_t stream) {
   if (lay.partition != kBlk || lay.head_dim != kD || args.group < 1 || args.group > 8) return hipErrorInvalidValue;
