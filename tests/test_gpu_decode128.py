@@ -159,3 +159,26 @@ def test_p128_exports_and_prefill_report_unsupported():
         hk.hack_debug_qk_products(case.layout, case.cache, torch.from_numpy(case.q).to(gu.DEV), case.lens_dev,
                                   case.max_len)
     assert e.value.status == 2
+
+
+@pytest.mark.parametrize("bits", [2, 4])
+def test_full_size_p128_decode_sampled(bits):
+    """decode_llama8b_l4096's shapes at partition 128 (batch 16, 32/8 heads, 4096
+    tokens, x10 outliers on 4 K channels), in the launch configuration the partition
+    sweep times: outputs of sampled rows against the oracle, and the split-K merge
+    over the full chunk count."""
+    hk, gu = _env()
+    gu.announce(f"full-size p128 decode bits={bits} (sampled)")
+    case = gu.Case(1128 + bits, 16, 8, [4096] * 16, bits, 128, group=4, outliers=4).quantize()
+    out = hk.hack_attend_decode(case.layout, case.cache, torch.from_numpy(case.q).to(gu.DEV), case.lens_dev, 4096)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    pairs = {(0, 0), (7, 4), (15, 7)}
+    seqs = case.oracle_seqs(pairs)
+    rows = [(b, h * 4 + g) for (b, h) in pairs for g in range(4)]
+    ref = O.attend_decode(case.q, seqs, 8, rows=rows)
+    got_rows = np.stack([got[b, h] for b, h in rows])
+    ref_rows = np.stack([ref[b, h] for b, h in rows])
+    err = float(np.abs(got_rows - ref_rows).max() / np.abs(ref_rows).max())
+    print(f"sampled rows max|d|/|O|inf = {err:.3e}")
+    assert err <= TOL
