@@ -286,7 +286,8 @@ __global__ __launch_bounds__(256, occupancy128<BITS>()) void decode128_kernel(De
     }
 
     // ---- softmax with a lazily raised reference max; P codes per (head, block) ----
-    float ps[kHeads], pm[kHeads], pz[kHeads];
+    float ps[kHeads], pm[kHeads];
+    int pz[kHeads];  // wave-uniform integer sums stay in scalar registers
 #pragma unroll
     for (int h = 0; h < kHeads; ++h) {
       if (h >= Gl) break;
@@ -303,7 +304,7 @@ __global__ __launch_bounds__(256, occupancy128<BITS>()) void decode128_kernel(De
       l_run[h] += p0 + p1;
       ps[h] = 0.0f;
       pm[h] = 0.0f;
-      pz[h] = 0.0f;
+      pz[h] = 0;
       if (vq) {
         const bool ok0 = tb + lane < L, ok1 = tb + 64 + lane < L;
         const float bmin = wave_min(fminf(ok0 ? sc[h][0] : INFINITY, ok1 ? sc[h][1] : INFINITY));
@@ -328,7 +329,7 @@ __global__ __launch_bounds__(256, occupancy128<BITS>()) void decode128_kernel(De
         }
         ps[h] = dp * a.inv_qmax;
         pm[h] = pmin;
-        pz[h] = (float)wave_sum_i(cd[0] + cd[1]);  // sum of p~' = p' - qoff over the block
+        pz[h] = wave_sum_i(cd[0] + cd[1]);  // sum of p~' = p' - qoff over the block
       } else if (v16) {
         p_tail[wave][h][lane] = p0;
         p_tail[wave][h][64 + lane] = p1;
@@ -354,15 +355,19 @@ __global__ __launch_bounds__(256, occupancy128<BITS>()) void decode128_kernel(De
       for (int h = 0; h < kHeads; ++h) {
         if (h >= Gl) break;
         // s_p s_v D~ + (s_p sum p~') m_v + m~_p (s_v sum v' + n m_v)
-        const float spz = ps[h] * pz[h], mtp = fmaf((float)qoff, ps[h], pm[h]);
+        const float spz = ps[h] * (float)pz[h], mtp = fmaf((float)qoff, ps[h], pm[h]);
         o0[h] += fmaf(ps[h] * sv[0], (float)dv[h][0], fmaf(spz, mv[0], mtp * vbar[0]));
         o1[h] += fmaf(ps[h] * sv[1], (float)dv[h][1], fmaf(spz, mv[1], mtp * vbar[1]));
       }
     } else if (v16) {
-      // fp16 open block: sum_t p_t v_t with unquantized p
-      const __half* vt = c.v_tail + ((int64_t)s * H + hkv) * kBlk * kD + 2 * lane;
+      // fp16 open block: sum_t p_t v_t with unquantized p.  The lane's byte offset is
+      // opaque to the compiler, so its address is formed here rather than hoisted
+      // out of the block loop (where it would stay live, and spill, for every wave).
+      uint32_t lo = 4u * (uint32_t)lane;
+      asm volatile("" : "+v"(lo));
+      const uint8_t* vt = reinterpret_cast<const uint8_t*>(c.v_tail + ((int64_t)s * H + hkv) * kBlk * kD) + lo;
       for (int e = 0; e < T; ++e) {
-        const float2 v = __half22float2(*reinterpret_cast<const __half2*>(vt + (int64_t)e * kD));
+        const float2 v = __half22float2(*reinterpret_cast<const __half2*>(vt + (uint32_t)e * (kD * 2)));
 #pragma unroll
         for (int h = 0; h < kHeads; ++h) {
           if (h >= Gl) break;
