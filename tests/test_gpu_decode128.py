@@ -182,3 +182,26 @@ def test_full_size_p128_decode_sampled(bits):
     err = float(np.abs(got_rows - ref_rows).max() / np.abs(ref_rows).max())
     print(f"sampled rows max|d|/|O|inf = {err:.3e}")
     assert err <= TOL
+
+
+@pytest.mark.parametrize("bits,tail", [(2, 0), (4, 1)])
+def test_p128_long_context_sampled(bits, tail):
+    """Partition 128 at the long-context size: batch 2, 8/2 heads, 131072 + 77 tokens
+    (chunks of 64 spans, an open block of 77 tokens), one sampled pair per sequence."""
+    hk, gu = _env()
+    L = 131072 + 77
+    gu.announce(f"long-context p128 bits={bits} tail={tail} L={L}")
+    case = gu.Case(1300 + bits, 2, 2, [L, L - 200], bits, 128, group=4).quantize()
+    out = hk.hack_attend_decode(case.layout, case.cache, torch.from_numpy(case.q).to(gu.DEV), case.lens_dev,
+                                case.max_len, tail)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    pairs = {(0, 1), (1, 0)}
+    seqs = case.oracle_seqs(pairs)
+    rows = [(b, h * 4 + g) for (b, h) in pairs for g in range(4)]
+    ref = O.attend_decode(case.q, seqs, 2, 8, tail, rows=rows)
+    got_rows = np.stack([got[b, h] for b, h in rows])
+    ref_rows = np.stack([ref[b, h] for b, h in rows])
+    err = float(np.abs(got_rows - ref_rows).max() / np.abs(ref_rows).max())
+    print(f"sampled rows max|d|/|O|inf = {err:.3e}")
+    assert err <= TOL
