@@ -123,6 +123,15 @@ __device__ __forceinline__ uint32_t sum_codes(const uint32_t* x) {
   return s;
 }
 
+// two floats as one 8-byte word (first in the low half) and back
+__device__ __forceinline__ uint64_t pack2(float lo, float hi) {
+  return (uint64_t)__float_as_uint(lo) | ((uint64_t)__float_as_uint(hi) << 32);
+}
+__device__ __forceinline__ void unpack2(uint64_t w, float& lo, float& hi) {
+  lo = __uint_as_float((uint32_t)w);
+  hi = __uint_as_float((uint32_t)(w >> 32));
+}
+
 template <int N>
 __device__ __forceinline__ void load_dwords(const uint8_t* p, uint32_t* x) {
 #pragma unroll
@@ -417,14 +426,11 @@ __global__ __launch_bounds__(256, occupancy128<BITS>()) void decode128_kernel(De
       o[0] = x0 * inv;
       o[1] = x1 * inv;
     } else {
-      // agent-coherent (write-through) stores, complete once the store counter drains
-      float* rec = a.partials + ((pair * a.splits + split) * G + head0 + gh) * REC;
-      if (ch == 0) {
-        __hip_atomic_store(rec, mmax, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(rec + 1, lsum, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      }
-      __hip_atomic_store(rec + 4 + ch, x0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(rec + 5 + ch, x1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      // agent-coherent (write-through) 8-byte stores, complete once the store counter
+      // drains; a record is 8-byte aligned (528 bytes each from a 256-byte base)
+      uint64_t* rec = reinterpret_cast<uint64_t*>(a.partials + ((pair * a.splits + split) * G + head0 + gh) * REC);
+      if (ch == 0) __hip_atomic_store(rec, pack2(mmax, lsum), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(rec + 2 + ch / 2, pack2(x0, x1), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
   if (nsplit == 1) return;
@@ -448,11 +454,10 @@ __global__ __launch_bounds__(256, occupancy128<BITS>()) void decode128_kernel(De
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         if (sp0 + u < nsplit) {
-          const float* rec = a.partials + ((pair * a.splits + sp0 + u) * G + head0 + gh) * REC;
-          ms[u] = __hip_atomic_load(rec, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          ls[u] = __hip_atomic_load(rec + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          xa[u] = __hip_atomic_load(rec + 4 + ch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          xb[u] = __hip_atomic_load(rec + 5 + ch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          const uint64_t* rec =
+              reinterpret_cast<const uint64_t*>(a.partials + ((pair * a.splits + sp0 + u) * G + head0 + gh) * REC);
+          unpack2(__hip_atomic_load(rec, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT), ms[u], ls[u]);
+          unpack2(__hip_atomic_load(rec + 2 + ch / 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT), xa[u], xb[u]);
         } else {
           ms[u] = -INFINITY;
           ls[u] = 0.0f;
