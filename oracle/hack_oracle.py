@@ -22,7 +22,7 @@ Precision: the quantizer of stored K/V and of Q uses float32 operations in a
 fixed order (so the codes are single-valued); every product and correction is
 int64 / float64.  P is quantized in float64.
 
-Readings where the paper is silent or garbled (each also listed in the design doc):
+Readings where the paper is silent or garbled:
   R1  bits b general: scale = (max-min)/(2^b-1) (the text writes 2^2-1).
   R2  stored scale is the float32 scale rounded *up* to fp16 so that
       (max-min)/s <= 2^b-1; min is stored exactly (it is an input value).
