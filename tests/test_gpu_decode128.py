@@ -33,6 +33,9 @@ CASES = [
     (4, 6, 1, [2048 + 17, 400], 1, 1024, 8),
     (2, 4, 2, [256, 1, 127, 129, 600], 0, 0, 4),
     (4, 8, 2, [77, 129, 1000], 1, 0, 4),
+    (2, 3, 1, [1, 2, 3], 0, 0, 8),
+    (4, 5, 1, [128 * 7, 1], 1, 0, 8),
+    (2, 7, 2, [512, 513, 1023], 2, 1024, 8),
 ]
 
 
@@ -205,3 +208,57 @@ def test_p128_long_context_sampled(bits, tail):
     err = float(np.abs(got_rows - ref_rows).max() / np.abs(ref_rows).max())
     print(f"sampled rows max|d|/|O|inf = {err:.3e}")
     assert err <= TOL
+
+
+def test_p128_split_merge_sees_each_calls_records():
+    """Back-to-back partition-128 decode calls on one workspace with alternating
+    queries and several chunks per sequence: the merging workgroup must read the
+    current call's records, and every call leaves the counters at zero."""
+    hk, gu = _env()
+    gu.announce("p128 split-K merge over repeated calls")
+    case = gu.Case(1808, 4, 2, [2000, 1999, 1500, 2048], 2, 128, group=4).quantize()
+    qa = case.q
+    qb = gu.synth.normal_f16(1809, "q", qa.shape)
+    seqs = case.oracle_seqs()
+    refs = [O.attend_decode(q, seqs, case.H, 8, 0) for q in (qa, qb)]
+    qd = [torch.from_numpy(q).to(gu.DEV) for q in (qa, qb)]
+    ws = hk.decode_workspace(case.layout, case.batch, case.Hq, case.max_len)
+    outs = [torch.empty((case.batch, case.Hq, case.d), dtype=torch.float32, device=gu.DEV) for _ in range(40)]
+    for it, out in enumerate(outs):  # queued back to back, no host synchronization in between
+        hk.hack_attend_decode(case.layout, case.cache, qd[it % 2], case.lens_dev, case.max_len, out=out, workspace=ws)
+    torch.cuda.synchronize()
+    for it, out in enumerate(outs):
+        err = gu.rel_err(out.cpu().numpy(), refs[it % 2])
+        assert err <= TOL, f"call {it}: {err:.3e}"
+    nbytes = hk.hack_decode_workspace_bytes(case.layout, case.batch, case.Hq, case.max_len)
+    counters = ws.view(torch.uint8)[:nbytes].cpu().numpy()
+    # the counters follow the 256-byte aligned records; all are back at zero
+    B, H, G = case.batch, case.H, case.G
+    assert not np.any(counters[nbytes - ((B * H * ((G + 3) // 4) * 4 + 255) // 256) * 256:])
+
+
+def test_p128_decode_step_paged():
+    """hack_decode_step at partition 128 on a paged cache (512-token pages): same bytes
+    and outputs as append then decode."""
+    hk, gu = _env()
+    lens = [510, 511, 1023, 40]
+    gu.announce(f"decode step p128 paged lens={lens}")
+    a = gu.Case(1811, len(lens), 2, lens, 2, 128, group=4, paged_page=512, spare_tokens=3).quantize()
+    b = gu.Case(1811, len(lens), 2, lens, 2, 128, group=4, paged_page=512, spare_tokens=3).quantize()
+    lens_in, lens_out = b.lens_dev.clone(), torch.zeros_like(b.lens_dev)
+    for step in range(3):
+        cur = a.lens_dev.cpu().numpy()
+        kn = torch.from_numpy(np.stack([a.k[s, :, cur[s]] for s in range(a.batch)])).to(gu.DEV)
+        vn = torch.from_numpy(np.stack([a.v[s, :, cur[s]] for s in range(a.batch)])).to(gu.DEV)
+        q = torch.from_numpy(gu.synth.normal_f16(1900 + step, "q", (a.batch, a.Hq, a.d))).to(gu.DEV)
+        ml = int(cur.max())
+        hk.hack_append(a.layout, a.cache, kn, vn, a.lens_dev, ml, 1)
+        ref_out = hk.hack_attend_decode(a.layout, a.cache, q, a.lens_dev, ml + 1, 1)
+        got = hk.hack_decode_step(b.layout, b.cache, kn, vn, q, lens_in, lens_out, ml, 1)
+        torch.cuda.synchronize()
+        assert torch.equal(lens_out, a.lens_dev)
+        assert torch.equal(got, ref_out)
+        lens_in, lens_out = lens_out, lens_in
+    ra, rb = a.sections(), b.sections()
+    for name in ra:
+        assert np.array_equal(ra[name], rb[name]), name
