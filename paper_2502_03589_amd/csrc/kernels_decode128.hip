@@ -233,22 +233,19 @@ __global__ __launch_bounds__(256, occupancy128<BITS>()) void decode128_kernel(De
   const int nblk = (t1 - t0 + kBlk - 1) / kBlk;
   int8_t* pb = reinterpret_cast<int8_t*>(&p_op[wave][0][0]);
 
-  for (int bi = wave; bi < nblk; bi += kWaves128) {
-    const int tb = t0 + bi * kBlk;  // chunks start at multiples of the block
-    const int kb = tb / kBlk;
-    const bool vq = kb < F || (codes_open && kb == F && T > 0);  // V read from codes
-    const bool v16 = !codes_open && kb == F && T > 0;            // fp16 open block
-    const int nb = kb < F ? kBlk : T;                            // tokens of the block
-    // a block never crosses a page (pages hold whole decode spans of 4 blocks)
-    const int64_t krow = k_row(c, s, hkv, tb);
-    const int64_t vblk = v_block<kBlk>(c, s, hkv, tb);
-
-    // ---- K rows of tokens lane and 64 + lane ----
-    uint32_t kc[2][KD], km[2], kz[2];
+  // K rows of tokens lane and 64 + lane of the block starting at token tbx.  With
+  // cached sums a wave requests its next block's rows as soon as the current scores
+  // are computed, so they arrive while it runs the softmax and P'V' of the current
+  // block (1-3% faster); rebuilding the sums from the codes keeps more registers live
+  // there, and the prefetch would spill, so that variant loads each block's rows at
+  // its start.
+  uint32_t kc[2][KD], km[2], kz[2];
+  auto load_k = [&](int tbx) __attribute__((always_inline)) {
+    const int64_t krow = k_row(c, s, hkv, tbx);  // a block never crosses a page
 #pragma unroll
     for (int r = 0; r < 2; ++r) {
       const int e = 64 * r + lane;
-      if (tb + e < L) {
+      if (tbx + e < L) {
         load_dwords<KD>(c.k_codes + (krow + e) * (kD * BITS / 8), kc[r]);
         km[r] = reinterpret_cast<const uint32_t*>(c.k_meta)[krow + e];
         kz[r] = SE ? (uint32_t)reinterpret_cast<const uint16_t*>(c.k_sums)[krow + e] : 0u;
@@ -259,6 +256,20 @@ __global__ __launch_bounds__(256, occupancy128<BITS>()) void decode128_kernel(De
         kz[r] = 0u;
       }
     }
+  };
+  if constexpr (SE) {
+    if (wave < nblk) load_k(t0 + wave * kBlk);
+  }
+
+  for (int bi = wave; bi < nblk; bi += kWaves128) {
+    const int tb = t0 + bi * kBlk;  // chunks start at multiples of the block
+    const int kb = tb / kBlk;
+    const bool vq = kb < F || (codes_open && kb == F && T > 0);  // V read from codes
+    const bool v16 = !codes_open && kb == F && T > 0;            // fp16 open block
+    const int nb = kb < F ? kBlk : T;                            // tokens of the block
+    // a block never crosses a page (pages hold whole decode spans of 4 blocks)
+    const int64_t vblk = v_block<kBlk>(c, s, hkv, tb);
+    if constexpr (!SE) load_k(tb);
 
     // ---- Q'K' and Eq. 4 per (head, token) ----
     float sc[kHeads][2];
@@ -271,6 +282,9 @@ __global__ __launch_bounds__(256, occupancy128<BITS>()) void decode128_kernel(De
     }
     int dq[kHeads][2] = {{0, 0}, {0, 0}, {0, 0}, {0, 0}};
     dot_rows<BITS, KD>(kc[0], kc[1], &q_op[0][0], 32, Gl, dq);
+    if constexpr (SE) {
+      if (bi + kWaves128 < nblk) load_k(tb + kWaves128 * kBlk);  // the K registers are free now
+    }
 #pragma unroll
     for (int h = 0; h < kHeads; ++h) {
       if (h >= Gl) break;
