@@ -1,13 +1,16 @@
 """Benchmark of the quantized-KV attention hot path on one MI355X.
 
-Default workload: Llama-3-8B-shaped decode (batch 16, 32 q heads / 8 kv heads,
-head_dim 128, context 4096, 2-bit K/V with partition 32, 4 K channels x10).
-One step = one hack_decode_step launch: quantize-on-write of one new token per
-(sequence, kv head) fused with decode attention over the whole compressed cache.
-Ten replicas of the cache rotate so that the 256 MB Infinity Cache cannot hold the
-working set.  Also measured: causal prefill (batch 1, 32/8 heads, 8192 tokens,
-4-bit K/V, partition 64).  --workload selects another decode workload instead
-(ragged paged 70B share, 128K append loop, or the bit-width/partition sweep).
+Headline workload: the 70B-shaped one-GPU decode share (batch 64, 64 q heads / 8 kv
+heads, head_dim 128, per-request context uniform in [1024, 32768], 256-token pages,
+2-bit K/V with partition 32).  One step = one hack_decode_step: quantize-on-write of
+one new token per (sequence, kv head) fused with decode attention over the whole
+compressed cache (0.88 GB, beyond the 256 MB Infinity Cache, so no replicas are
+needed).  Also measured, each with its own roofline: the Llama-3-8B-shaped decode
+(batch 16, 32/8 heads, context 4096, 4 K channels x10; ten cache replicas), the
+128K-context append loop (batch 4, 32/8 heads, 2- and 4-bit), the single small decode
+(launch-latency bound), causal prefill (batch 1, 32/8 heads, 8192 tokens, 4-bit K/V,
+partition 64) and quantize-on-write of a prompt.  The oracle is timed on the host's
+cores over a bounded sample of the headline workload, before the GPU is touched.
 
 Prints ONE JSON line.  `value` is compressed bytes moved per step / step time.
 """
@@ -88,27 +91,6 @@ def profiled_traffic(kernel_file: str, summary: str):
         return None
 
 
-VALU_PEAK_LANE_OPS = 16 * 4 * 256 * 2.4e9  # 16 lanes x 4 SIMDs x 256 CUs x 2.4 GHz (unpacked fp32)
-
-
-def profiled_field(kernel_file: str, summary: str, field: str, sha_field: str = "kernel_source_sha256"):
-    """An integer field of a committed rocprofv3 summary, or None when the kernel source
-    has changed since the summary was taken."""
-    import hashlib
-    try:
-        text = open(os.path.join(ROOT, "profiles", summary)).read()
-        src = open(os.path.join(ROOT, "paper_2502_03589_amd", "csrc", kernel_file), "rb").read()
-    except OSError:
-        return None
-    fields = dict(line.split(": ", 1) for line in text.splitlines() if ": " in line and not line.startswith(" "))
-    if fields.get(sha_field, "").strip() != hashlib.sha256(src).hexdigest():
-        return None
-    try:
-        return int(fields[field])
-    except (KeyError, ValueError):
-        return None
-
-
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -123,9 +105,9 @@ def parse():
                     default=None,
                     help="time another decode workload instead (one JSON line per configuration; "
                          "not the headline line)")
-    ap.add_argument("--only", choices=["decode", "prefill", "copy"], default=None,
-                    help="profiling aid: run one leg alone (copy = plain device copy of a known size, "
-                         "the calibration for HBM byte counters)")
+    ap.add_argument("--only", choices=["decode", "llama8b", "long", "prefill", "copy", "cpu"], default=None,
+                    help="profiling aid: run one leg alone (decode = the headline 70B-share decode step; "
+                         "copy = plain device copy of a known size, the calibration for HBM byte counters)")
     return ap.parse_args()
 
 
@@ -160,66 +142,176 @@ def copy_bandwidth(mib: int = 1024, iters: int = 10) -> float:
     return 2 * (mib << 20) / (ms * 1e-3) / 1e9
 
 
-def cpu_baseline_decode(wl, budget_s: float = 15.0):
-    """The oracle timed on host cores over a bounded sample of the decode workload:
-    whole (sequence, kv head) pairs at the full context, all G query heads each."""
+# ---------------------------------------------------------------------------------
+# Oracle baseline on the host cores (run before the GPU is initialised)
+# ---------------------------------------------------------------------------------
+def _oracle_worker(pairs, barrier, results, slot):
+    """Times the oracle's decode attention (G query rows over L tokens) for each
+    (sequence, kv head, L) of `pairs`, after building their quantized caches untimed.
+    All workers start their timed section together (barrier)."""
     from threadpoolctl import threadpool_limits
 
     from oracle import hack_oracle as O
     from paper_2502_03589_amd import synth
-    d, L, G = wl.head_dim, wl.context, wl.group
-    ch = synth.outlier_channels(wl.seed, d, wl.outlier_channels)
-    pairs, bytes_done, t_used = 0, 0, 0.0
-    sb = O.sum_bytes(wl.kv_bits, wl.partition)
-    while t_used < budget_s and pairs < wl.batch * wl.kv_heads:
-        b, h = divmod(pairs, wl.kv_heads)
-        k = synth.scale_channels_f16(synth.normal_f16(wl.seed, "k", (L, d), sub=1 + pairs), ch, 10.0)
-        v = synth.normal_f16(wl.seed, "v", (L, d), sub=1 + pairs)
-        q = synth.normal_f16(wl.seed, "q", (G, d), sub=1 + pairs)
-        sq = O.quantize_sequence(k, v, wl.kv_bits, wl.partition)
-        with threadpool_limits(1):  # numpy's BLAS on one thread, as reported in `cores`
-            t0 = time.perf_counter()
+    wl = synth.WORKLOADS["decode_70b_ragged"]
+    d, G, H = wl.head_dim, wl.group, wl.kv_heads
+    with threadpool_limits(1):
+        prepared = []
+        per_seq = {}
+        for b, h, L in pairs:
+            if b not in per_seq:
+                per_seq = {b: (synth.normal_f16(wl.seed, "k", (1, H, L, d), sub=1 + b),
+                               synth.normal_f16(wl.seed, "v", (1, H, L, d), sub=1 + b))}
+            k, v = per_seq[b]
+            sq = O.quantize_sequence(k[0, h], v[0, h], wl.kv_bits, wl.partition)
+            q = synth.normal_f16(wl.seed, "q", (1, H * G, d))[0, h * G:(h + 1) * G]
+            prepared.append((sq, q, L))
+        per_seq = None
+        if barrier is not None:
+            barrier.wait()
+        t0 = time.perf_counter()
+        nbytes = 0
+        sb = O.sum_bytes(wl.kv_bits, wl.partition)
+        for sq, q, L in prepared:
             for g in range(G):
                 O.decode_row(q[g], sq)
-            t_used += time.perf_counter() - t0
-        bytes_done += decode_bytes_per_seq_head(L, d, wl.kv_bits, wl.partition, sb) + G * d * (2 + 4)
-        pairs += 1
-    return {"value": round(bytes_done / t_used / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": f"{pairs} of {wl.batch * wl.kv_heads} (sequence, kv head) pairs at context {L}, "
-                      f"{G} query heads each; {t_used:.1f} s single-threaded numpy"}
+            nbytes += decode_bytes_per_seq_head(L, d, wl.kv_bits, wl.partition, sb) + G * d * (2 + 4)
+        dt = time.perf_counter() - t0
+    if results is not None:
+        results[slot] = (nbytes, dt)
+    return nbytes, dt
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the decode path shards by "
-              f"(sequence, kv head) with no communication, so N GPUs run N independent copies.",
-              file=sys.stderr)
-        sys.exit(2)
-    if args.only == "copy":
-        copy_calibration()
-        return
-    if args.workload is not None:
-        bench_workload(args.workload, args.steps, args.warmup)
-        return
-    if args.only == "prefill":
-        print(json.dumps({"prefill": bench_prefill(args.prefill_iters)}), flush=True)
-        return
+def cpu_baseline_decode(pairs_per_core: int = 6):
+    """The oracle on every host core: one forked worker per core, each timing the
+    decode attention of `pairs_per_core` whole (sequence, kv head) pairs of the headline
+    workload (lengths from the same seeded draw); aggregate rate = all bytes / the
+    slowest worker's timed span.  Also one worker alone on one core, as a second figure."""
+    import multiprocessing as mp
+
+    from paper_2502_03589_amd import synth
+    wl = synth.WORKLOADS["decode_70b_ragged"]
+    lens = synth.uniform_lengths(wl.seed, wl.batch, *wl.len_range)
+    cores = len(os.sched_getaffinity(0))
+    all_pairs = [(b, h, int(lens[b])) for b in range(wl.batch) for h in range(wl.kv_heads)]
+    n = min(len(all_pairs), cores * pairs_per_core)
+    ctx = mp.get_context("fork")  # no GPU state exists yet in this process
+    one_b, one_t = _oracle_worker(all_pairs[:pairs_per_core], None, None, 0)
+    barrier = ctx.Barrier(cores)
+    results = ctx.Manager().dict()
+    procs = [ctx.Process(target=_oracle_worker, args=(all_pairs[w:n:cores], barrier, results, w))
+             for w in range(cores)]
+    for pr in procs:
+        pr.start()
+    for pr in procs:
+        pr.join()
+    if any(pr.exitcode != 0 for pr in procs) or len(results) != cores:
+        return {"status": "oracle workers failed"}
+    tot_b = sum(v[0] for v in results.values())
+    span = max(v[1] for v in results.values())
+    lsum = sum(int(L) for _, _, L in all_pairs[:n])
+    return {"value": round(tot_b / span / 1e9, 4), "unit": "GB/s", "cores": cores, "kind": "oracle",
+            "sample": f"decode attention of {n} of {len(all_pairs)} (sequence, kv head) pairs of decode_70b_ragged "
+                      f"({lsum} cached tokens, {wl.group} query rows each, inputs quantized untimed), "
+                      f"{cores} forked workers of single-threaded numpy, {span:.1f} s wall",
+            "single_core": {"value": round(one_b / one_t / 1e9, 4), "unit": "GB/s", "cores": 1,
+                            "sample": f"first {pairs_per_core} pairs, {one_t:.1f} s"}}
+
+
+# ---------------------------------------------------------------------------------
+# GPU legs
+# ---------------------------------------------------------------------------------
+def roofline_hbm(kernel: str, step_bytes: float, avg_kern_ms: float, kernel_file: str, counters: str):
+    achieved = step_bytes / (avg_kern_ms * 1e-3) / 1e9
+    return {"bound": "hbm", "kernel": kernel, "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
+            "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": profiled_traffic(kernel_file, counters),
+            "avg_kernel_us": round(avg_kern_ms * 1e3, 3), "bytes_per_launch": int(step_bytes)}
+
+
+def run_steps(step, step_bytes_at, warmup: int, steps: int, stream):
+    """Warm up, then time `steps` steps: wall clock (host, synchronized on both sides)
+    and HIP events recorded on the launch stream around the queued launches."""
+    import torch
+    for i in range(warmup):
+        step(i)
+    nbytes = sum(step_bytes_at(warmup + j) for j in range(steps))
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for j in range(steps):
+        step(warmup + j)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    return nbytes / steps, (t1 - t0) * 1e3 / steps, ev0.elapsed_time(ev1) / steps
+
+
+def bench_ragged(steps: int, warmup: int):
+    """Headline: decode steps (append one token + attend) on the 70B-shaped share."""
     import torch
     from paper_2502_03589_amd import hack as hk
     from paper_2502_03589_amd import synth
-
     dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
+    wl = synth.WORKLOADS["decode_70b_ragged"]
+    B, Hq, H, d, pi, pt = wl.batch, wl.q_heads, wl.kv_heads, wl.head_dim, wl.partition, wl.page_tokens
+    total = warmup + steps
+    lens = synth.uniform_lengths(wl.seed, B, *wl.len_range)
+    # each sequence gets pages for its prompt plus every token the steps append
+    table, pages = synth.page_table(wl.seed, lens, pt, spare_pages=(total + pt - 1) // pt)
+    lay = hk.hack_kv_layout_make(d, H, wl.kv_bits, pi, pt)
+    cache = hk.KVCache(lay, pages, B, torch.from_numpy(table).to(dev), dev)
+    lens_a = torch.from_numpy(lens.copy()).to(dev)
+    for b in range(B):
+        L = int(lens[b])
+        k = torch.from_numpy(synth.normal_f16(wl.seed, "k", (1, H, L, d), sub=1 + b)).to(dev)
+        v = torch.from_numpy(synth.normal_f16(wl.seed, "v", (1, H, L, d), sub=1 + b)).to(dev)
+        hk.hack_quantize(lay, cache.sequences(b, 1), k, v, lens_a[b:b + 1], L)
+    del k, v
+    nk = torch.from_numpy(synth.normal_f16(wl.seed, "step_k", (8, B, H, d))).to(dev)
+    nv = torch.from_numpy(synth.normal_f16(wl.seed, "step_v", (8, B, H, d))).to(dev)
+    qs = torch.from_numpy(synth.normal_f16(wl.seed, "q", (8, B, Hq, d))).to(dev)
+    lens_b = torch.zeros_like(lens_a)
+    max_len = int(lens.max()) + total - 1  # bounds the lengths before any of the steps
+    ws = hk.decode_workspace(lay, B, Hq, max_len + 1)
+    out = torch.empty((B, Hq, d), dtype=torch.float32, device=dev)
+    calls = [[hk.bind_decode_step(lay, cache, nk[r], nv[r], qs[r], src, dst, max_len, hk.TAIL_FP16, out, ws)
+              for src, dst in ((lens_a, lens_b), (lens_b, lens_a))] for r in range(8)]
+    stream = torch.cuda.current_stream()
+    sb = lay.sum_bytes
+
+    def step(i):
+        calls[i % 8][i % 2](stream)
+
+    def step_bytes_at(i):
+        dec = sum(H * decode_bytes_per_seq_head(int(L) + i + 1, d, wl.kv_bits, pi, sb) for L in lens)
+        app = sum(append_bytes(1, H, d, wl.kv_bits, pi, sb, (int(L) + i + 1) % pi) for L in lens)
+        return dec + B * Hq * d * (2 + 4) + app
+
+    step_bytes, ms, kern_ms = run_steps(step, step_bytes_at, warmup, steps, stream)
+    cfg = {"workload": "decode_70b_ragged", "batch": B, "q_heads": Hq, "kv_heads": H, "head_dim": d,
+           "context": f"uniform [{wl.len_range[0]}, {wl.len_range[1]}] per request ({int(lens.sum())} tokens)",
+           "page_tokens": pt, "kv_bits": wl.kv_bits, "partition": pi, "qp_bits": 8,
+           "step": "append 1 token per (sequence, kv head) + decode attention (one launch)",
+           "parallelism": "1 GPU"}
+    roof = roofline_hbm("decode_kernel (hack_decode_step: append + attention + split-K merge)", step_bytes,
+                        kern_ms, "kernels_decode.hip", "decode_70b_ragged_hbm_counters.txt")
+    return step_bytes, ms, cfg, roof
+
+
+def bench_llama8b(steps: int, warmup: int, R: int):
+    """Decode steps on the Llama-3-8B-shaped workload over R cache replicas."""
+    import torch
+    from paper_2502_03589_amd import hack as hk
+    from paper_2502_03589_amd import synth
+    dev = torch.device("cuda:0")
     wl = synth.WORKLOADS["decode_llama8b_l4096"]
     B, Hq, H, d, L0 = wl.batch, wl.q_heads, wl.kv_heads, wl.head_dim, wl.context
-    bits, pi, R = wl.kv_bits, wl.partition, args.replicas
-    total_steps = args.warmup + args.steps
-    grow = (total_steps + R - 1) // R
+    bits, pi = wl.kv_bits, wl.partition
+    grow = (warmup + steps + R - 1) // R
     cap = ((L0 + grow + pi - 1) // pi) * pi
     lay = hk.hack_kv_layout_make(d, H, bits, pi, cap)
-
-    # inputs: K with 4 outlier channels x10, V, the new tokens and the queries
     ch = synth.outlier_channels(wl.seed, d, wl.outlier_channels)
     k = torch.from_numpy(synth.scale_channels_f16(synth.normal_f16(wl.seed, "k", (B, H, L0, d)), ch, 10.0)).to(dev)
     v = torch.from_numpy(synth.normal_f16(wl.seed, "v", (B, H, L0, d))).to(dev)
@@ -243,12 +335,6 @@ def main():
     q_gbs = quantize_bytes(B, H, L0, d, bits, pi, sb) / (q_ms * 1e-3) / 1e9
     del k, v
     out = torch.empty((B, Hq, d), dtype=torch.float32, device=dev)
-
-    # One step = append one token per (sequence, kv head) (quantize-on-write) + decode
-    # attention, fused in one launch (hack_decode_step).  The calls are bound once
-    # (arguments marshalled up front) so the host runs ahead of the GPU; the length
-    # arrays of a replica alternate between input and output; max_len arguments are
-    # upper bounds (the kernels read the true lengths from device memory).
     stream = torch.cuda.current_stream()
     lens2 = [torch.zeros_like(x) for x in lens]
     ws = hk.decode_workspace(lay, B, Hq, cap)
@@ -263,34 +349,130 @@ def main():
         parity[r] ^= 1
 
     def step_bytes_at(i):
-        """Algorithmic bytes of step i: the replica's cache grows by one token per step."""
         Lr = L0 + i // R + 1
         dec = B * H * decode_bytes_per_seq_head(Lr, d, bits, pi, sb) + B * Hq * d * (2 + 4)
         return dec + append_bytes(B, H, d, bits, pi, sb, Lr % pi)
 
-    for i in range(args.warmup):
-        step(i)
-    nbytes = sum(step_bytes_at(args.warmup + j) for j in range(args.steps))
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    ev0.record(stream)
-    for j in range(args.steps):
-        step(args.warmup + j)
-    ev1.record(stream)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ms_per_step = (t1 - t0) * 1e3 / args.steps
-    # the timed region holds nothing but the step launches: the events' span per step
-    # is the step kernel's average duration (launches queue back to back)
-    avg_kern_ms = ev0.elapsed_time(ev1) / args.steps
-    step_bytes = nbytes / args.steps
-    value = step_bytes / (ms_per_step * 1e-3) / 1e9
-    achieved = step_bytes / (avg_kern_ms * 1e-3) / 1e9
+    step_bytes, ms, kern_ms = run_steps(step, step_bytes_at, warmup, steps, stream)
+    res = {"workload": "decode_llama8b_l4096", "step": "append 1 token + decode attention (one launch)",
+           "cache_replicas": R, "ms_per_step": round(ms, 5), "GBs": round(step_bytes / (ms * 1e-3) / 1e9, 2),
+           "roofline": roofline_hbm("decode_kernel (hack_decode_step)", step_bytes, kern_ms,
+                                    "kernels_decode.hip", "decode_llama8b_l4096_hbm_counters.txt")}
+    quant = {"workload": "decode_llama8b_l4096 prompt (hack_quantize of 16 x 8 x 4096 tokens)",
+             "ms": round(q_ms, 4), "GBs": round(q_gbs, 1), "frac_hbm": round(q_gbs / HBM_PEAK_GBS, 4)}
+    return res, quant
 
+
+def bench_long(bits_list=(2, 4)):
+    """The 128K-context loop: after quantizing 131072 tokens per sequence, 64 steps of
+    (append one token per (sequence, kv head), decode attention), fp16 open block."""
+    import torch
+    from paper_2502_03589_amd import hack as hk
+    from paper_2502_03589_amd import synth
+    dev = torch.device("cuda:0")
+    wl = synth.WORKLOADS["decode_long_l131072"]
+    B, Hq, H, d, pi = wl.batch, wl.q_heads, wl.kv_heads, wl.head_dim, wl.partition
+    L0, nsteps = wl.context, wl.steps
+    cap = L0 + nsteps
+    k_all = torch.from_numpy(np.stack([synth.normal_f16(wl.seed, "k", (H, cap, d), sub=1 + b) for b in range(B)])).to(dev)
+    v_all = torch.from_numpy(np.stack([synth.normal_f16(wl.seed, "v", (H, cap, d), sub=1 + b) for b in range(B)])).to(dev)
+    qs = torch.from_numpy(np.stack([synth.normal_f16(wl.seed, "q", (B, Hq, d), sub=1 + i) for i in range(nsteps)])).to(dev)
+    knew = [k_all[:, :, L0 + i].contiguous() for i in range(nsteps)]
+    vnew = [v_all[:, :, L0 + i].contiguous() for i in range(nsteps)]
+    k0, v0 = k_all[:, :, :L0].contiguous(), v_all[:, :, :L0].contiguous()
+    del k_all, v_all
+    stream = torch.cuda.current_stream()
+    res = {}
+    for bits in bits_list:
+        lay = hk.hack_kv_layout_make(d, H, bits, pi, cap)
+        cache = hk.KVCache(lay, B, B, None, dev)
+        lens = torch.full((B,), L0, dtype=torch.int32, device=dev)
+        lens2 = torch.zeros_like(lens)
+        ws = hk.decode_workspace(lay, B, Hq, cap)
+        out = torch.empty((B, Hq, d), dtype=torch.float32, device=dev)
+        calls = [hk.bind_decode_step(lay, cache, knew[i], vnew[i], qs[i], *((lens, lens2) if i % 2 == 0 else (lens2, lens)),
+                                     cap - 1, hk.TAIL_FP16, out, ws) for i in range(nsteps)]
+        sb = lay.sum_bytes
+
+        def step_bytes_at(i):
+            dec = B * H * decode_bytes_per_seq_head(L0 + i + 1, d, bits, pi, sb) + B * Hq * d * 6
+            return dec + append_bytes(B, H, d, bits, pi, sb, (L0 + i + 1) % pi)
+
+        # pass 0 warms the kernels up; both passes start from the same quantized prefix
+        for timed_pass in (False, True):
+            lens.fill_(L0)
+            hk.hack_quantize(lay, cache, k0, v0, lens, L0)
+            step_bytes, ms, kern_ms = run_steps(lambda i: calls[i](stream), step_bytes_at, 0, nsteps, stream)
+        res[f"b{bits}"] = {"kv_bits": bits, "steps": nsteps, "tail_mode": "fp16", "ms_per_step": round(ms, 5),
+                           "GBs": round(step_bytes / (ms * 1e-3) / 1e9, 2),
+                           "roofline": roofline_hbm("decode_kernel (hack_decode_step)", step_bytes, kern_ms,
+                                                    "kernels_decode.hip", f"decode_long_l131072_b{bits}_hbm_counters.txt")}
+        del cache, ws
+    return res
+
+
+def bench_tiny(steps: int = 200, warmup: int = 20):
+    """One decode call of batch 1, one q / kv head, 256 tokens: launch-latency sized."""
+    import torch
+    from paper_2502_03589_amd import hack as hk
+    from paper_2502_03589_amd import synth
+    dev = torch.device("cuda:0")
+    wl = synth.WORKLOADS["decode_tiny_l256"]
+    B, Hq, H, d, pi, L, R = wl.batch, wl.q_heads, wl.kv_heads, wl.head_dim, wl.partition, wl.context, 64
+    lay = hk.hack_kv_layout_make(d, H, wl.kv_bits, pi, L)
+    k = torch.from_numpy(synth.normal_f16(wl.seed, "k", (B, H, L, d))).to(dev)
+    v = torch.from_numpy(synth.normal_f16(wl.seed, "v", (B, H, L, d))).to(dev)
+    q = torch.from_numpy(synth.normal_f16(wl.seed, "q", (B, Hq, d))).to(dev)
+    ln = torch.full((B,), L, dtype=torch.int32, device=dev)
+    caches = [hk.KVCache(lay, B, B, None, dev) for _ in range(R)]
+    for cache in caches:
+        hk.hack_quantize(lay, cache, k, v, ln, L)
+    ws = hk.decode_workspace(lay, B, Hq, L)
+    out = torch.empty((B, Hq, d), dtype=torch.float32, device=dev)
+    calls = [hk.bind_attend_decode(lay, cache, q, ln, L, hk.TAIL_FP16, out, ws) for cache in caches]
+    stream = torch.cuda.current_stream()
+    nbytes = B * H * decode_bytes_per_seq_head(L, d, wl.kv_bits, pi, lay.sum_bytes) + B * Hq * d * 6
+    _, ms, kern_ms = run_steps(lambda i: calls[i % R](stream), lambda i: nbytes, warmup, steps, stream)
+    return {"workload": "decode_tiny_l256", "us_per_call": round(kern_ms * 1e3, 2), "bytes_per_call": int(nbytes),
+            "note": "back-to-back calls; launch-latency bound, a fraction of HBM peak is not meaningful"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the decode path shards by "
+              f"(sequence, kv head) with no communication, so N GPUs run N independent copies.",
+              file=sys.stderr)
+        sys.exit(2)
+    # the oracle baseline forks worker processes: before anything initialises the GPU
+    cpu = None
+    if not args.no_cpu_baseline and args.only in (None, "cpu"):
+        cpu = cpu_baseline_decode()
+        if args.only == "cpu":
+            print(json.dumps({"cpu_baseline": cpu}), flush=True)
+            return
+    if args.only == "copy":
+        copy_calibration()
+        return
+    if args.workload is not None:
+        bench_workload(args.workload, args.steps, args.warmup)
+        return
+    if args.only == "prefill":
+        print(json.dumps({"prefill": bench_prefill(args.prefill_iters)}), flush=True)
+        return
+    if args.only == "llama8b":
+        print(json.dumps({"decode_llama8b_l4096": bench_llama8b(args.steps, args.warmup, args.replicas)[0]}), flush=True)
+        return
+    if args.only == "long":
+        print(json.dumps({"decode_long_l131072": bench_long()}), flush=True)
+        return
+    import torch
+    torch.cuda.set_device(torch.device("cuda:0"))
+
+    step_bytes, ms_per_step, cfg, roof = bench_ragged(args.steps, args.warmup)
     result = {
         "metric": "decode: compressed-KV GB/s (append + attend per step)",
-        "value": round(value, 2),
+        "value": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 2),
         "unit": "GB/s",
         "n_gpus": 1,
         "steps": args.steps,
@@ -301,28 +483,22 @@ def main():
         "vs_baseline": None,
         "dtype": "int8",
         "data": "synthetic",
-        "config": {"workload": "decode_llama8b_l4096", "batch": B, "q_heads": Hq, "kv_heads": H,
-                   "head_dim": d, "context": L0, "kv_bits": bits, "partition": pi, "qp_bits": 8,
-                   "outlier_k_channels": wl.outlier_channels, "cache_replicas": R,
-                   "step": "append 1 token + decode attention (one launch)", "parallelism": "1 GPU"},
-        "roofline": {"bound": "hbm", "kernel": "decode_kernel (hack_decode_step: append + attention + split-K merge)",
-                     "achieved": round(achieved, 2),
-                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": profiled_traffic("kernels_decode.hip", "decode_llama8b_l4096_hbm_counters.txt"),
-                     "avg_kernel_us": round(avg_kern_ms * 1e3, 3),
-                     "bytes_per_launch": int(step_bytes)},
-        "box_copy_GBs": round(copy_bandwidth(), 1),
-        "quantize": {"workload": "decode_llama8b_l4096 prompt (hack_quantize of 16 x 8 x 4096 tokens)",
-                     "ms": round(q_ms, 4), "GBs": round(q_gbs, 1), "frac_hbm": round(q_gbs / HBM_PEAK_GBS, 4)},
+        "config": cfg,
+        "roofline": roof,
     }
-    if not args.no_prefill and args.only is None:
-        result["prefill"] = bench_prefill(args.prefill_iters)
-        # the same workload with 4-bit Q/P codes (the literal reading of its 4-bit Q/K/V/P)
-        result["prefill_qp4"] = bench_prefill(max(3, args.prefill_iters // 2), 4)
-        # the paper's rounding: stochastic K/V, Q and P codes
-        result["prefill_stochastic"] = bench_prefill(max(3, args.prefill_iters // 2), 8, 1)
-    if not args.no_cpu_baseline and args.only is None:
-        result["cpu_baseline"] = cpu_baseline_decode(wl)
+    if args.only is None:
+        result["decode_llama8b_l4096"], result["quantize"] = bench_llama8b(args.steps, args.warmup, args.replicas)
+        result["decode_long_l131072"] = bench_long()
+        result["decode_tiny_l256"] = bench_tiny()
+        result["box_copy_GBs"] = round(copy_bandwidth(), 1)
+        if not args.no_prefill:
+            result["prefill"] = bench_prefill(args.prefill_iters)
+            # the same workload with 4-bit Q/P codes (the literal reading of its 4-bit Q/K/V/P)
+            result["prefill_qp4"] = bench_prefill(max(3, args.prefill_iters // 2), 4)
+            # the paper's rounding: stochastic K/V, Q and P codes
+            result["prefill_stochastic"] = bench_prefill(max(3, args.prefill_iters // 2), 8, 1)
+        if cpu is not None:
+            result["cpu_baseline"] = cpu
     print(json.dumps(result), flush=True)
 
 
@@ -350,14 +526,15 @@ def bench_prefill(iters: int, qp_bits: int = 8, rounding: int = 0):
         return {"status": f"unavailable: {e}"}
     torch.cuda.synchronize()
     ops = 2 * Hq * (L * (L + 1) // 2) * d * 2 * B
+    stream = torch.cuda.current_stream()
     e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
     qt, at = [], []
     for _ in range(iters):
-        e0.record()
+        e0.record(stream)
         hk.hack_quantize(lay, c, k, v, ln, L)
-        e1.record()
+        e1.record(stream)
         hk.hack_attend_prefill(lay, c, q, True, out)
-        e2.record()
+        e2.record(stream)
         torch.cuda.synchronize()
         qt.append(e0.elapsed_time(e1))
         at.append(e1.elapsed_time(e2))
@@ -365,21 +542,12 @@ def bench_prefill(iters: int, qp_bits: int = 8, rounding: int = 0):
     q_ms = float(np.median(qt))
     tops = ops / (a_ms * 1e-3) / 1e12
     q_gbs = quantize_bytes(B, H, L, d, wl.kv_bits, wl.partition, lay.sum_bytes) / (q_ms * 1e-3) / 1e9
-    res = {"workload": "prefill_l8192", "qp_bits": qp_bits, "rounding": "stochastic" if rounding else "nearest",
-           "int8_ops": ops, "attend_ms": round(a_ms, 4),
-           "quantize_ms": round(q_ms, 4), "quantize_GBs": round(q_gbs, 1), "TOPS": round(tops, 2),
-           "peak_TOPS": INT8_PEAK_TOPS, "frac": round(tops / INT8_PEAK_TOPS, 4)}
-    if qp_bits == 8 and rounding == 0:
-        # the path is bound by its VALU work: VALU lane-operations per second (profiled
-        # instruction count x 64 lanes over the measured time) against the VALU peak
-        n = profiled_field("kernels_prefill.hip", "prefill_l8192_valu_mfma_counters.txt", "prefill_valu_instructions_per_launch",
-                           "prefill_kernel_source_sha256")
-        if n is not None:
-            ach = n * 64 / (a_ms * 1e-3) / 1e12
-            res["alu_roofline"] = {"bound": "alu", "achieved": round(ach, 2), "peak": round(VALU_PEAK_LANE_OPS / 1e12, 1),
-                                   "unit": "T VALU lane-ops/s", "frac": round(ach * 1e12 / VALU_PEAK_LANE_OPS, 4),
-                                   "valu_instructions_per_launch": n}
-    return res
+    return {"workload": "prefill_l8192", "qp_bits": qp_bits, "rounding": "stochastic" if rounding else "nearest",
+            "int8_ops": ops, "attend_ms": round(a_ms, 4),
+            "quantize_ms": round(q_ms, 4), "quantize_GBs": round(q_gbs, 1),
+            "roofline": {"bound": "mfma", "kernel": "prefill_kernel", "achieved": round(tops, 2),
+                         "peak": INT8_PEAK_TOPS, "unit": "TOPS (int8)", "frac": round(tops / INT8_PEAK_TOPS, 4),
+                         "traffic": None}}
 
 
 def bench_workload(name: str, steps: int, warmup: int):

@@ -45,21 +45,26 @@ typedef enum hack_status {
   HACK_ERR_HIP = 5               /* the HIP runtime rejected a launch              */
 } hack_status;
 
-/* Rounding of stored K/V codes (Sec. 5.2).  STOCHASTIC rounds t up with
- * probability frac(t); its thresholds are u = (SplitMix64(seed ^ (stream<<56) ^ idx)
- * >> 40) * 2^-24 with stream 1 for K, 2 for V and idx = ((seq*H_kv + head) * 2^32 +
- * token) * head_dim + channel.  Q and P are always rounded to nearest-even. */
+/* Rounding of every code the library produces (Sec. 5.2): the stored K/V codes
+ * (hack_quantize, hack_append, hack_decode_step) and the transient Q and P codes inside
+ * the attention kernels.  NEAREST_EVEN rounds t = (x - min) / scale to the nearest
+ * integer, ties to even.  STOCHASTIC rounds t up with probability frac(t): the code is
+ * floor(t) + [u < t - floor(t)] with u = (SplitMix64(seed ^ (stream << 56) ^ idx) >> 40)
+ * * 2^-24.  Streams and element indices:
+ *   K 1, V 2: idx = ((seq*H_kv + head) * 2^32 + token) * head_dim + channel;
+ *   Q 3, P 4: idx = ((seq*H_q + q_head) * 2^20 + row) * 2^24 + column, where row is the
+ *             query row (0 in decode) and column the Q channel or the P key token. */
 enum { HACK_ROUND_NEAREST_EVEN = 0, HACK_ROUND_STOCHASTIC = 1 };
 
 /* Treatment of the open (last, partial) V block of T = len mod Pi tokens (Sec. 5.3):
- * FP16    - kept in fp16 and multiplied with the unquantized P (the paper's default);
- * REQUANT - re-quantized from its fp16 originals with n = T on every append, and
- *           multiplied through Eq. 4 with n = T. */
-/* Open V block modes (Sec. 5.3): FP16 keeps it in fp16 (requantization elimination,
- * the paper's default); REQUANT re-quantizes it from its fp16 values on every append;
- * DEQUANT re-quantizes it from its dequantized codes plus the new value on every
- * append (the alternative the paper's requantization elimination replaces, whose
- * rounding errors accumulate).  REQUANT and DEQUANT attend over the block's codes. */
+ * FP16    - kept in fp16 and multiplied with the unquantized P (requantization
+ *           elimination, the paper's default);
+ * REQUANT - re-quantized from its fp16 originals (kept in V_TAIL) with n = T on every
+ *           append, and multiplied through Eq. 4 with n = T;
+ * DEQUANT - re-quantized on every append from its dequantized codes plus the new value
+ *           (the alternative that requantization elimination replaces; its rounding
+ *           errors accumulate), and multiplied through Eq. 4 with n = T.
+ * A cache is attended with the mode it was appended with. */
 enum { HACK_TAIL_FP16 = 0, HACK_TAIL_REQUANT = 1, HACK_TAIL_DEQUANT = 2 };
 
 /* Device arrays of a quantized KV cache.  Let P = head_dim/partition,
@@ -165,10 +170,11 @@ hack_status hack_append(const hack_kv_layout* layout, const hack_kv_cache* cache
                         const void* k_new_dev, const void* v_new_dev, int32_t* seq_lens_dev,
                         int32_t batch, int32_t max_len, int32_t tail_mode, hipStream_t stream);
 
-/* Workspace bytes hack_attend_decode needs for these sizes (the split-K partial
- * results: max, sum and unnormalized O per chunk and query head, and one counter per
- * (sequence, kv head)).  -1 on invalid
- * arguments. */
+/* Workspace bytes hack_attend_decode needs for these sizes.  Layout: one int32
+ * chunk counter per (sequence, kv head, group of four query heads) at offset 0, padded
+ * to 256 bytes, then the split-K chunk records (max, sum and unnormalized O per chunk
+ * and query head).  The counters' place and size depend only on batch, H_kv and
+ * H_q/H_kv, never on max_len.  -1 on invalid arguments. */
 int64_t hack_decode_workspace_bytes(const hack_kv_layout* layout, int32_t batch,
                                     int32_t num_q_heads, int32_t max_len);
 
@@ -177,11 +183,13 @@ int64_t hack_decode_workspace_bytes(const hack_kv_layout* layout, int32_t batch,
  * attends kv head h / (H_q/H_kv).  Per sequence, all seq_lens[s] cached tokens are
  * attended (0 <= seq_lens[s] <= max_len; a sequence of length 0 yields zeros).
  * out_dev: fp32 [batch][H_q][head_dim].  workspace_dev must hold
- * hack_decode_workspace_bytes(...) bytes, must be zero-filled before its first use
- * (every call leaves it that way: it holds per-sequence chunk counters next to the
- * chunk records) and must not be shared by calls that may run concurrently.  One
- * kernel is launched; when a sequence is split into several chunks, the workgroup
- * that finishes its last chunk merges them.
+ * hack_decode_workspace_bytes(...) bytes.  Its counters (the first bytes, see
+ * hack_decode_workspace_bytes) must be zero before the first call, and again before
+ * a call with a different batch, H_q or layout; every call leaves them zero, so a
+ * workspace may be reused by calls that differ only in max_len.  A workspace must not
+ * be shared by calls that may run concurrently.  One kernel is launched; when a
+ * sequence is split into several chunks, the workgroup that finishes its last chunk
+ * merges them.
  * Requires head_dim 128, partition 32, 64 or 128, H_q/H_kv <= 8, batch <= 65535 and,
  * for a paged cache, page_tokens a multiple of 4 * partition (else
  * HACK_ERR_UNSUPPORTED).  Partitions of 32 and 64 run on the matrix cores; a
@@ -201,9 +209,11 @@ hack_status hack_attend_decode(const hack_kv_layout* layout, const hack_kv_cache
  * arrays must be distinct (callers swap them between steps).  max_len bounds
  * seq_lens_in; max_len + 1 must not exceed the capacity (HACK_ERR_CAPACITY).  The
  * workspace is the one hack_decode_workspace_bytes(layout, batch, H_q, max_len + 1)
- * sizes, zero-filled before first use as for hack_attend_decode.  With partition
- * 128 the step is three operations on the stream (a copy of the lengths, the append
- * kernel, the attention kernel), else one launch. */
+ * sizes, with its counters zeroed as for hack_attend_decode.  The step is one launch,
+ * except with partition 128, and in DEQUANT mode when H_q/H_kv > 4 (the kv group then
+ * spans several workgroups, and one kernel must requantize the open block before any
+ * of them reads it): then it is three operations on the stream (a copy of the
+ * lengths, the append kernel, the attention kernel). */
 hack_status hack_decode_step(const hack_kv_layout* layout, const hack_kv_cache* cache,
                              const void* k_new_dev, const void* v_new_dev, const void* q_dev,
                              int32_t num_q_heads, const int32_t* seq_lens_in_dev,

@@ -81,6 +81,15 @@ hack::DecodePlan plan_attend(const hack_kv_layout& l, int batch, int num_q_heads
                             : hack::plan_decode(l, batch, num_q_heads, max_len);
 }
 
+// Points the split-K fields of `a` at a workspace laid out as `plan` describes:
+// chunk counters at offset 0, chunk records after them.
+void bind_workspace(hack::DecodeArgs& a, const hack::DecodePlan& plan, void* ws) {
+  a.counters = static_cast<int32_t*>(ws);
+  a.partials = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + plan.record_offset);
+  a.chunk = plan.chunk;
+  a.splits = plan.splits;
+}
+
 hipError_t launch_attend(const hack_kv_layout& l, const hack::DecodeArgs& a, int batch, hipStream_t stream) {
   if (l.partition == 128) return hack::launch_decode128(l, a, batch, stream);
   return hack::launch_decode(l, a, batch, hack::MODE_ATTEND, stream);
@@ -216,10 +225,7 @@ hack_status hack_attend_decode(const hack_kv_layout* layout, const hack_kv_cache
   if (!workspace_dev || workspace_bytes < plan.workspace_bytes) return HACK_ERR_WORKSPACE;
   if (batch == 0) return HACK_OK;
   a.out = out_dev;
-  a.partials = static_cast<float*>(workspace_dev);
-  a.counters = reinterpret_cast<int32_t*>(static_cast<uint8_t*>(workspace_dev) + plan.counter_offset);
-  a.chunk = plan.chunk;
-  a.splits = plan.splits;
+  bind_workspace(a, plan, workspace_dev);
   a.tail_requant = tail_mode;  // 0: fp16 open block; 1, 2: its codes (re-quantized on append)
   (void)hipGetLastError();
   return from_hip(launch_attend(*layout, a, batch, stream));
@@ -243,10 +249,7 @@ hack_status hack_decode_step(const hack_kv_layout* layout, const hack_kv_cache* 
   if (!workspace_dev || workspace_bytes < plan.workspace_bytes) return HACK_ERR_WORKSPACE;
   if (batch == 0) return HACK_OK;
   a.out = out_dev;
-  a.partials = static_cast<float*>(workspace_dev);
-  a.counters = reinterpret_cast<int32_t*>(static_cast<uint8_t*>(workspace_dev) + plan.counter_offset);
-  a.chunk = plan.chunk;
-  a.splits = plan.splits;
+  bind_workspace(a, plan, workspace_dev);
   a.tail_requant = tail_mode;  // 0: fp16 open block; 1, 2: its codes (re-quantized on append)
   a.k_new = static_cast<const __half*>(k_new_dev);
   a.v_new = static_cast<const __half*>(v_new_dev);
@@ -256,10 +259,18 @@ hack_status hack_decode_step(const hack_kv_layout* layout, const hack_kv_cache* 
   a.key_k = layout->seed ^ (1ull << 56);
   a.key_v = layout->seed ^ (2ull << 56);
   (void)hipGetLastError();
-  if (layout->partition == 128) {
-    // The partition-128 kernel attends only: the new lengths start as a copy of the
-    // old ones, the append kernel writes the token and bumps them, and the attention
-    // reads them (three operations on the stream instead of one launch).
+  // In the fused launch every workgroup whose chunk holds the new token appends it.
+  // That is safe while those workgroups write identical bytes computed from the fp16
+  // originals (FP16, REQUANT).  In DEQUANT mode the append reads the open block's codes
+  // back and rewrites them, so when a kv group is split over several workgroups (more
+  // than four query heads) one of them could requantize a block another has already
+  // requantized.  That case, like partition 128 (whose attention kernel does not
+  // append), runs the append as its own kernel first.
+  const bool separate_append = layout->partition == 128 || (tail_mode == HACK_TAIL_DEQUANT && plan.head_groups > 1);
+  if (separate_append) {
+    // The new lengths start as a copy of the old ones, the append kernel writes the
+    // token and bumps them, and the attention reads them (three operations on the
+    // stream instead of one launch).
     if (layout->num_kv_heads * layout->head_dim > 2048) return HACK_ERR_UNSUPPORTED;  // one append workgroup
     hipError_t e = hipMemcpyAsync(seq_lens_out_dev, seq_lens_in_dev, (size_t)batch * sizeof(int32_t),
                                   hipMemcpyDeviceToDevice, stream);

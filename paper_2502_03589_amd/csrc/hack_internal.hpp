@@ -13,13 +13,29 @@ namespace hack {
 // Decode split plan: tokens per workgroup (a multiple of 4*partition) and the
 // number of splits of the longest sequence.  Depends only on the sizes, so the
 // workspace query and the attend call always agree.
+// Workspace layout: the chunk counters first, at offset 0, one int32 per
+// (sequence, kv head, head group), padded to 256 bytes; the chunk records after them.
+// The counters' place depends only on batch, H_kv and the group size, so a call with a
+// different max_len (hence a different split count) never lands its counters on an
+// earlier call's records.
 struct DecodePlan {
   int chunk;
   int splits;
+  int head_groups;          // workgroups per (sequence, kv head, chunk)
   int64_t partial_floats;   // batch * H_kv * splits * G * (4 + head_dim)
-  int64_t counter_offset;   // byte offset of the per-(sequence, kv head) counters
+  int64_t counter_bytes;    // batch * H_kv * head_groups int32 counters, padded to 256 bytes
+  int64_t record_offset;    // byte offset of the chunk records (= counter_bytes)
   int64_t workspace_bytes;
 };
+
+// Fills the layout fields of a plan from its chunk/split choice.
+inline void finish_plan(DecodePlan& p, int64_t pairs, int64_t group, int64_t head_groups, int64_t head_dim) {
+  p.head_groups = (int)head_groups;
+  p.partial_floats = pairs * p.splits * group * (4 + head_dim);
+  p.counter_bytes = ((pairs * head_groups * 4 + 255) / 256) * 256;
+  p.record_offset = p.counter_bytes;
+  p.workspace_bytes = p.record_offset + ((p.partial_floats * 4 + 255) / 256) * 256;
+}
 
 DecodePlan plan_decode(const hack_kv_layout& lay, int batch, int num_q_heads, int max_len);
 DecodePlan plan_decode128(const hack_kv_layout& lay, int batch, int num_q_heads, int max_len);

@@ -25,7 +25,8 @@
 //   open block  fp16 values times unquantized probabilities (TAIL_FP16), or its
 //         re-quantized codes with n = T (TAIL_REQUANT).
 // The four waves merge in LDS; when a sequence spans several chunks, each chunk's
-// partial (max, sum, O) goes to the workspace and a second, small kernel merges them.
+// partial (max, sum, O) goes to the workspace and the workgroup that finishes the
+// sequence's last chunk merges them in the same launch.
 #include <algorithm>
 #include <type_traits>
 
@@ -130,19 +131,6 @@ constexpr float kMaxSlack = 8.0f;
 constexpr int kWaves = 4;
 constexpr int kComputeUnits = 256;  // MI355X
 
-// Waves per SIMD of the 2-bit, partition-32, one-row-tile kernel, and whether it
-// stages V through LDS with direct loads (needed to fit 128 VGPRs at four waves).
-// Measured: two waves per SIMD with V in registers is faster.  The compiler cannot
-// order direct-to-LDS loads with ordinary ones, so with V in LDS every wave waits
-// for all of its span's loads (vmcnt 0) before its first Q'K' product; with plain
-// loads the Q'K' tiles start as their own K data arrives, overlapping the rest.
-#ifndef HACK_DECODE_FAST_OCC
-#define HACK_DECODE_FAST_OCC 2
-#endif
-#ifndef HACK_DECODE_V_DMA
-#define HACK_DECODE_V_DMA 0
-#endif
-
 
 // Bytes of one cached code sum: 1 when b + ceil(log2 PI) <= 8, else 2 (Sec. 5.3).
 template <int BITS, int PI>
@@ -152,26 +140,15 @@ constexpr int sum_width() {
   return need <= 8 ? 1 : 2;
 }
 
-// Waves per SIMD the register budget is sized for.  The 2-bit, partition-32
-// kernel with one row tile fits in 128 VGPRs (four waves per SIMD hide the load
-// latency of a span behind three others' arithmetic); wider spans and two row
-// tiles need more registers.
+// Waves per SIMD the register budget is sized for (the launch bound's minimum).
+// Measured: compiling for two waves per SIMD leaves the 2-bit, partition-32 kernel
+// at about 145 VGPRs, so three are resident; a cap for three (168 VGPRs) or four
+// (128 VGPRs, with V staged through LDS by direct loads) forced spills or a full
+// wait on every span's loads and was slower.
 template <int BITS, int PI, int GT>
 constexpr int decode_occupancy() {
-  return (BITS == 2 && PI == 32 && GT == 1) ? HACK_DECODE_FAST_OCC : 2;
+  return 2;
 }
-
-#ifndef HACK_DECODE_FUSED_MERGE
-#define HACK_DECODE_FUSED_MERGE 2  // 1/2: the last chunk of a sequence merges (else a second launch)
-#endif
-
-#ifndef HACK_DECODE_SPAN_ROUND
-#define HACK_DECODE_SPAN_ROUND 1
-#endif
-
-#ifndef HACK_DECODE_WGS_PER_CU
-#define HACK_DECODE_WGS_PER_CU 0  // 0: the kernel's occupancy
-#endif
 
 // Section bases of a span: its four V blocks are consecutive blocks of one page.
 struct SpanBase {
@@ -223,28 +200,6 @@ struct SpanData {
   uint32_t vz[2 * SB];    // cached V code sums of those channels, packed
 };
 
-// V of one span staged in LDS by direct global->LDS loads: copy i of the codes
-// holds bytes [16i, 16i+16) of every lane's run, lane-major, so that each lane
-// reads its own 16-byte pieces back without bank conflicts.
-template <int BITS, int PI>
-struct VStage {
-  static constexpr int VW = PI * BITS / 32;
-  static constexpr int SB = sum_width<BITS, PI>();
-  static constexpr int NC = 8 * VW / 4;               // 16-byte pieces of V codes per lane
-  static constexpr int ZB = SB == 1 ? 4 : 16;         // bytes per sum piece
-  static constexpr int NZ = 8 * SB / ZB;              // sum pieces per lane
-  uint8_t codes[NC][64 * 16];
-  uint8_t meta[2][64 * 16];
-  uint8_t sums[NZ][64 * ZB];
-};
-
-// Whether a kernel stages V through LDS (the four-waves-per-SIMD configuration,
-// whose register budget cannot also hold a span's V data).
-template <int BITS, int PI, int GT>
-constexpr bool decode_v_in_lds() {
-  return decode_occupancy<BITS, PI, GT>() == 4 && HACK_DECODE_V_DMA;
-}
-
 // LDS of one wave.
 template <int BITS, int PI, int GT>
 struct WaveLds {
@@ -254,33 +209,17 @@ struct WaveLds {
   float alpha[GT][4];           // O rescale of the span, per head
   float tailf[GT][4];           // scale of the fp16 open block's probabilities
   float ptail[GT][4][PI];       // unquantized p~ of the open block
-  // the wave's V staging; after its last span the wave's partial O reuses the space
-  union {
-    VStage<BITS, PI> vst[decode_v_in_lds<BITS, PI, GT>() ? 1 : 0];
-    float mrg_o[HT][128];
-  };
+  float mrg_o[HT][128];          // the wave's partial O after its last span
 };
-
-__device__ __forceinline__ void lds_dma16(const uint8_t* src, uint8_t* lds) {
-  __builtin_amdgcn_global_load_lds((__attribute__((address_space(1))) const void*)src,
-                                   (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
-}
-__device__ __forceinline__ void lds_dma4(const uint8_t* src, uint8_t* lds) {
-  __builtin_amdgcn_global_load_lds((__attribute__((address_space(1))) const void*)src,
-                                   (__attribute__((address_space(3))) void*)lds, 4, 0, 0);
-}
 
 // Split-K merge of one (sequence, kv head): combines the partial (max, sum, O) of
 // its nsplit chunks with a running max and writes O / sum.  The records of all
 // planned chunks are read together (records past the sequence are stale and are
 // masked by the length), so the caller waits on memory once per group of U chunks.
-template <bool COHERENT>
 __device__ __forceinline__ float ld_rec(const float* p) {
-  if constexpr (COHERENT) return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  else return *p;
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-template <bool COHERENT>
 __device__ __forceinline__ void merge_chunks(const DecodeArgs& a, int s, int hkv, int Lraw, int head0, int Gl) {
   constexpr int D = 128, REC = 4 + D, U = 8;
   const int G = a.group, Hq = a.num_q_heads;
@@ -296,18 +235,11 @@ __device__ __forceinline__ void merge_chunks(const DecodeArgs& a, int s, int hkv
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         if (sp0 + u < a.splits) {
+          // agent-coherent loads: the records were written by other workgroups
           const float* rec = a.partials + ((pair * a.splits + sp0 + u) * G + gh) * REC;
-          if constexpr (COHERENT) {
-            ms[u] = ld_rec<true>(rec);
-            ls[u] = ld_rec<true>(rec + 1);
-            os[u] = float4{ld_rec<true>(rec + 4 + ch), ld_rec<true>(rec + 5 + ch), ld_rec<true>(rec + 6 + ch),
-                           ld_rec<true>(rec + 7 + ch)};
-          } else {
-            const float2 ml = *reinterpret_cast<const float2*>(rec);
-            ms[u] = ml.x;
-            ls[u] = ml.y;
-            os[u] = *reinterpret_cast<const float4*>(rec + 4 + ch);
-          }
+          ms[u] = ld_rec(rec);
+          ls[u] = ld_rec(rec + 1);
+          os[u] = float4{ld_rec(rec + 4 + ch), ld_rec(rec + 5 + ch), ld_rec(rec + 6 + ch), ld_rec(rec + 7 + ch)};
         } else {
           ms[u] = -INFINITY;
           ls[u] = 0.0f;
@@ -367,7 +299,6 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
   // the byte order of the K operand's in-register unpack
   __shared__ __attribute__((aligned(16))) int8_t q_lds[HT][4][2][16];
   __shared__ float qm_lds[HT][4][3];
-  constexpr bool VLDS = decode_v_in_lds<BITS, PI, GT>();
   __shared__ __attribute__((aligned(16))) WaveLds<BITS, PI, GT> wl_all[kWaves];
   __shared__ float mrg_ml[kWaves][HT][2];
 
@@ -567,22 +498,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
     const int vkb = vbt0 / PI;
     bool gvalid = full || (vbt0 < L && (vkb < F || (requant && vkb == F && T > 0)));
     if constexpr (MODE == MODE_PV) gvalid = vbt0 < L && vkb < F;
-    if constexpr (VLDS) {
-      // straight into this wave's LDS; lanes of blocks that are not read leave
-      // their slots stale and zero their values when reading them back
-      using VS = VStage<BITS, PI>;
-      if (gvalid) {
-#pragma unroll
-        for (int i = 0; i < VS::NC; ++i) lds_dma16(b.vc + o_vc + 16 * i, wl.vst[0].codes[i]);
-#pragma unroll
-        for (int i = 0; i < 2; ++i) lds_dma16(b.vm + o_vm + 16 * i, wl.vst[0].meta[i]);
-#pragma unroll
-        for (int i = 0; i < (SE ? VS::NZ : 0); ++i) {
-          if constexpr (VS::ZB == 4) lds_dma4(b.vz + o_vz + 4 * i, wl.vst[0].sums[i]);
-          else lds_dma16(b.vz + o_vz + 16 * i, wl.vst[0].sums[i]);
-        }
-      }
-    } else if (gvalid) {
+    if (gvalid) {
       load_words<8 * VW>(b.vc + o_vc, d.vc);
       load_words<8>(b.vm + o_vm, d.vm);
       if constexpr (SE) {
@@ -785,38 +701,9 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
 
     // ---------------- P'V' and Eq. 4: lane (channel col, group = block k) ----------------
     {
-      uint32_t vcr[8 * VW], vmr[8], vzr[2 * SB];
-      if constexpr (VLDS) {
-        using VS = VStage<BITS, PI>;
-        // the direct-to-LDS loads of this span have landed once vmcnt is zero
-        __builtin_amdgcn_s_waitcnt(0x0F70);
-#pragma unroll
-        for (int i = 0; i < VS::NC; ++i) {
-          const uint4 x = gvalid ? *reinterpret_cast<const uint4*>(&wl.vst[0].codes[i][16 * lane]) : uint4{0, 0, 0, 0};
-          vcr[4 * i] = x.x; vcr[4 * i + 1] = x.y; vcr[4 * i + 2] = x.z; vcr[4 * i + 3] = x.w;
-        }
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-          const uint4 x = gvalid ? *reinterpret_cast<const uint4*>(&wl.vst[0].meta[i][16 * lane]) : uint4{0, 0, 0, 0};
-          vmr[4 * i] = x.x; vmr[4 * i + 1] = x.y; vmr[4 * i + 2] = x.z; vmr[4 * i + 3] = x.w;
-        }
-#pragma unroll
-        for (int i = 0; i < VS::NZ; ++i) {
-          if constexpr (VS::ZB == 4) {
-            vzr[i] = gvalid ? *reinterpret_cast<const uint32_t*>(&wl.vst[0].sums[i][4 * lane]) : 0u;
-          } else {
-            const uint4 x = gvalid ? *reinterpret_cast<const uint4*>(&wl.vst[0].sums[i][16 * lane]) : uint4{0, 0, 0, 0};
-            vzr[4 * i] = x.x; vzr[4 * i + 1] = x.y; vzr[4 * i + 2] = x.z; vzr[4 * i + 3] = x.w;
-          }
-        }
-      } else {
-#pragma unroll
-        for (int w = 0; w < 8 * VW; ++w) vcr[w] = d.vc[w];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) vmr[j] = d.vm[j];
-#pragma unroll
-        for (int j = 0; j < 2 * SB; ++j) vzr[j] = d.vz[j];
-      }
+      const uint32_t* vcr = d.vc;
+      const uint32_t* vmr = d.vm;
+      const uint32_t* vzr = d.vz;
       const float n_g = (float)(vkb < F ? PI : T);
       const int kk = col >> 2, hh = col & 3;
       v4i pa[GT][TILES];
@@ -980,77 +867,48 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
       o[1] = o1 * inv;
     } else {
       float* rec = a.partials + ((pair * a.splits + split) * G + head0_e + gh) * REC;
-      if constexpr (HACK_DECODE_FUSED_MERGE == 2) {
-        // agent-coherent (write-through) stores: complete at the device's coherence
-        // point once the wave's store counter drains
-        if (ch == 0) {
-          __hip_atomic_store(rec, mmax, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          __hip_atomic_store(rec + 1, lsum, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-        __hip_atomic_store(rec + 4 + ch, o0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(rec + 5 + ch, o1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      } else {
-        if (ch == 0) {
-          rec[0] = mmax;
-          rec[1] = lsum;
-        }
-        rec[4 + ch] = o0;
-        rec[5 + ch] = o1;
+      // agent-coherent (write-through) stores: complete at the device's coherence
+      // point once the wave's store counter drains
+      if (ch == 0) {
+        __hip_atomic_store(rec, mmax, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(rec + 1, lsum, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
+      __hip_atomic_store(rec + 4 + ch, o0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(rec + 5 + ch, o1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
-#if HACK_DECODE_FUSED_MERGE
   if (MODE == MODE_ATTEND && nsplit > 1) {
     // The workgroup that finishes a sequence's last chunk merges all of them.
     __shared__ int last_chunk;
     __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's record stores are done
     __syncthreads();
     if (tid == 0) {
-#if HACK_DECODE_FUSED_MERGE == 2
+      // relaxed: the records are complete at the coherence point (vmcnt drained
+      // above), and the merger reads them with agent-coherent loads
       const int done = __hip_atomic_fetch_add(&a.counters[pair * a.head_groups + hg_e], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-#else
-      // acquire-release: publishes this chunk's record, and for the last arriver
-      // makes every other chunk's record visible
-      const int done = __hip_atomic_fetch_add(&a.counters[pair * a.head_groups + hg_e], 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-#endif
       last_chunk = done == nsplit - 1;
     }
     __syncthreads();
     if (last_chunk) {
-      merge_chunks<HACK_DECODE_FUSED_MERGE == 2>(a, s, hkv, L, head0_e, Gl_e);
+      merge_chunks(a, s, hkv, L, head0_e, Gl_e);
       if (tid == 0) __hip_atomic_store(&a.counters[pair * a.head_groups + hg_e], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
-#endif
-}
-
-// Split-K merge as a second launch: one workgroup per (sequence, kv head).
-__global__ __launch_bounds__(256) void decode_merge_kernel(DecodeArgs a) {
-  const int s = blockIdx.y, hkv = blockIdx.x;
-  const int Lraw = a.k_new != nullptr ? a.lens[s] + 1 : a.lens[s];  // a decode step attends lens + 1
-  const int L = max(0, min(Lraw, a.max_len));
-  if ((L + a.chunk - 1) / a.chunk <= 1) return;  // written directly by the attention kernel
-  merge_chunks<false>(a, s, hkv, Lraw, 0, a.group);
 }
 
 constexpr int64_t kMaxWgSpans = 64;
 constexpr int64_t kMaxGridZ = 65535;
 
+// Workgroups per (sequence, kv head, chunk): one per four query heads of the group.
+// (A two-row-tile workgroup for groups of 8 needed about 230 VGPRs, two waves per
+// SIMD, and was slower than two one-row-tile workgroups at three.)
+static int head_groups_of(int G) { return (G + 3) / 4; }
+
 // Workgroups per compute unit the grid is sized for.  The 2-bit, partition-32 kernel
-// with one row tile uses about 145 VGPRs, so three waves per SIMD are resident even
-// though it is compiled for two (measured best on the 4K-context decode workload).
-#ifndef HACK_DECODE_HEAD_SPLIT
-#define HACK_DECODE_HEAD_SPLIT 1  // groups of more than 4 heads: one-tile workgroups per 4 heads
-#endif
-
-// Row tiles (of 4 heads) per workgroup, and workgroups per (sequence, kv head, chunk).
-static int row_tiles_of(int G) { return (G <= 4 || HACK_DECODE_HEAD_SPLIT) ? 1 : 2; }
-static int head_groups_of(int G) { return (G + 4 * row_tiles_of(G) - 1) / (4 * row_tiles_of(G)); }
-
-static int occupancy_of(const hack_kv_layout& lay, int G) {
-  const int gt = row_tiles_of(G);
-  if (lay.kv_bits == 2 && lay.partition == 32 && gt == 1) return decode_occupancy<2, 32, 1>() + 1;
-  return 2;
+// uses about 145 VGPRs, so three waves per SIMD are resident even though it is
+// compiled for two (measured best on the 4K-context decode workload).
+static int occupancy_of(const hack_kv_layout& lay) {
+  return (lay.kv_bits == 2 && lay.partition == 32) ? 3 : 2;
 }
 
 DecodePlan plan_decode(const hack_kv_layout& lay, int batch, int num_q_heads, int max_len) {
@@ -1060,7 +918,7 @@ DecodePlan plan_decode(const hack_kv_layout& lay, int batch, int num_q_heads, in
   const int64_t G = lay.num_kv_heads > 0 ? num_q_heads / lay.num_kv_heads : 0;
   const int64_t nhg = G > 0 ? head_groups_of((int)G) : 1;
   // one workgroup per compute unit and resident wave slot of a SIMD
-  const int64_t per_cu = HACK_DECODE_WGS_PER_CU > 0 ? HACK_DECODE_WGS_PER_CU : occupancy_of(lay, (int)G);
+  const int64_t per_cu = occupancy_of(lay);
   const int64_t target = kComputeUnits * per_cu;
   const int64_t spans_seq = ((int64_t)max_len + span - 1) / span;
   int64_t wg_spans = pairs > 0 ? (spans_seq * pairs * nhg + target - 1) / target : 1;
@@ -1071,13 +929,9 @@ DecodePlan plan_decode(const hack_kv_layout& lay, int batch, int num_q_heads, in
   // stays within its 65535 limit.
   if (wg_spans > kMaxWgSpans) wg_spans = kMaxWgSpans;
   wg_spans = std::max<int64_t>(wg_spans, (spans_seq + kMaxGridZ - 1) / kMaxGridZ);
-  if (HACK_DECODE_SPAN_ROUND > 1 && wg_spans > kWaves)  // whole spans for every wave of a workgroup
-    wg_spans = (wg_spans + HACK_DECODE_SPAN_ROUND - 1) / HACK_DECODE_SPAN_ROUND * HACK_DECODE_SPAN_ROUND;
   p.chunk = (int)(wg_spans * span);
   p.splits = max_len > 0 ? (int)(((int64_t)max_len + p.chunk - 1) / p.chunk) : 1;
-  p.partial_floats = pairs * p.splits * G * (4 + lay.head_dim);
-  p.counter_offset = ((p.partial_floats * 4 + 255) / 256) * 256;
-  p.workspace_bytes = p.counter_offset + ((pairs * nhg * 4 + 255) / 256) * 256;
+  finish_plan(p, pairs, G, nhg, lay.head_dim);
   return p;
 }
 
@@ -1085,8 +939,6 @@ template <int BITS, int PI, int GT, int MODE, int QP, bool SE, bool SR = false>
 static hipError_t decode_impl(const DecodeArgs& a, int batch, hipStream_t stream) {
   dim3 grid((unsigned)(a.c.kv_heads * a.head_groups), (unsigned)batch, (unsigned)a.splits);
   hipLaunchKernelGGL((decode_kernel<BITS, PI, GT, MODE, QP, SE, SR>), grid, dim3(256), 0, stream, a);
-  if (MODE == MODE_ATTEND && a.splits > 1 && !HACK_DECODE_FUSED_MERGE)
-    hipLaunchKernelGGL(decode_merge_kernel, dim3((unsigned)a.c.kv_heads, (unsigned)batch), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 
@@ -1119,12 +971,7 @@ static hipError_t decode_gt(const DecodeArgs& args, int batch, int mode, hipStre
   if (args.group < 1 || args.group > 8) return hipErrorInvalidValue;
   DecodeArgs a = args;
   a.head_groups = head_groups_of(a.group);
-  if constexpr (HACK_DECODE_HEAD_SPLIT) {
-    return decode_qp<BITS, PI, 1>(a, batch, mode, stream);
-  } else {
-    if (row_tiles_of(a.group) == 1) return decode_qp<BITS, PI, 1>(a, batch, mode, stream);
-    return decode_qp<BITS, PI, 2>(a, batch, mode, stream);
-  }
+  return decode_qp<BITS, PI, 1>(a, batch, mode, stream);
 }
 
 hipError_t launch_decode(const hack_kv_layout& lay, const DecodeArgs& a, int batch, int mode,

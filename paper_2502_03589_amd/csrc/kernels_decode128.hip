@@ -540,9 +540,7 @@ DecodePlan plan_decode128(const hack_kv_layout& lay, int batch, int num_q_heads,
   wg_spans = std::max<int64_t>(wg_spans, (spans_seq + 65534) / 65535);
   p.chunk = (int)(wg_spans * span);
   p.splits = max_len > 0 ? (int)(((int64_t)max_len + p.chunk - 1) / p.chunk) : 1;
-  p.partial_floats = pairs * p.splits * G * (4 + kD);
-  p.counter_offset = ((p.partial_floats * 4 + 255) / 256) * 256;
-  p.workspace_bytes = p.counter_offset + ((pairs * nhg * 4 + 255) / 256) * 256;
+  finish_plan(p, pairs, G, nhg, kD);
   return p;
 }
 

@@ -40,34 +40,16 @@ constexpr int kRows = 32;        // query rows per workgroup (two 16-row MFMA ti
 constexpr float kScale = 0.12751743074941640f;  // log2(e) / sqrt(128)
 constexpr float kSlack = 8.0f;   // reference max raised only beyond this (log2 units)
 
-#ifndef HACK_PREFILL_SCALE_MFMA
-#define HACK_PREFILL_SCALE_MFMA 0  // s_q s_k and s_p s_v as outer-product MFMAs (else VALU)
-#endif
-#ifndef HACK_PREFILL_QK_RANK_MFMA
-#define HACK_PREFILL_QK_RANK_MFMA 1  // Q'K' rank-1 terms as outer-product MFMAs (else VALU)
-#endif
-#ifndef HACK_PREFILL_PV_RANK_MFMA
-#define HACK_PREFILL_PV_RANK_MFMA 0  // P'V' rank-1 terms as one outer-product MFMA per block
-#endif
-#ifndef HACK_PREFILL_PV_RANK_PAIRED
-#define HACK_PREFILL_PV_RANK_PAIRED 1  // ... as one outer-product MFMA per two blocks (else VALU)
-#endif
-
-#ifndef HACK_PREFILL_KPAD
-#define HACK_PREFILL_KPAD 32
-#endif
-#ifndef HACK_PREFILL_VPAD
-#define HACK_PREFILL_VPAD 32
-#endif
-
 template <int PI>
 struct PrefillCfg {
   static constexpr int D = 128;
   static constexpr int P = D / PI;    // K partitions per token
   static constexpr int TL = PI / 16;  // 16-token tiles per block
   static constexpr int KSL = PI / 4;  // operand bytes per lane per MFMA (k-slots of a lane group)
-  static constexpr int KROW = D + HACK_PREFILL_KPAD;  // LDS row stride of unpacked K (bytes)
-  static constexpr int VROW = PI + HACK_PREFILL_VPAD; // LDS row stride of unpacked V (bytes)
+  // LDS row strides of the unpacked K and V codes (bytes); the 32-byte pads were the
+  // best of a padding sweep of LDS bank conflicts
+  static constexpr int KROW = D + 32;
+  static constexpr int VROW = PI + 32;
 };
 
 // int8 MFMA with K = PI: 16x16x64 (16 bytes per lane) or 16x16x32 (8 bytes per lane).
@@ -395,16 +377,14 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
   }
 
   // Row-side operands of the outer-product MFMAs (lane (row, group g) supplies slot g):
-  // rank terms of partitions 2m, 2m+1 as (m~_q, R, m~_q, R); the scale s_q in slot 0.
-  float brank[(P + 1) / 2], bscale[P];
+  // rank terms of partitions 2m, 2m+1 as (m~_q, R, m~_q, R).
+  float brank[(P + 1) / 2];
 #pragma unroll
   for (int m = 0; m < (P + 1) / 2; ++m) {
     const int p = min(P - 1, 2 * m + (grp >> 1));
     const bool live = 2 * m + (grp >> 1) < P;
     brank[m] = live ? ((grp & 1) ? rq[p] : mq[p]) : 0.0f;
   }
-#pragma unroll
-  for (int p = 0; p < P; ++p) bscale[p] = grp == 0 ? sq[p] : 0.0f;
 
   float m_ref = -INFINITY, l_run = 0.0f;
   v4f o[8];
@@ -452,7 +432,6 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
       const int tt = 16 * tl + col;  // token of this lane's A-operand row
       // rank-1 terms summed over the partitions: token-side slot g = (partition, term)
       v4f s4 = v4f{0.0f, 0.0f, 0.0f, 0.0f};
-#if HACK_PREFILL_QK_RANK_MFMA
 #pragma unroll
       for (int m = 0; m < (P + 1) / 2; ++m) {
         const int p = min(P - 1, 2 * m + (grp >> 1));
@@ -460,32 +439,14 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
         const float ak = live ? st.km[p][1 + (grp & 1)][tt] : 0.0f;  // s_k sum k' | m_k
         s4 = mfma_f32(ak, brank[m], s4);
       }
-#else
-#pragma unroll
-      for (int p = 0; p < P; ++p) {
-        const float4 f1 = *reinterpret_cast<const float4*>(&st.km[p][1][16 * tl + 4 * grp]);
-        const float4 f2 = *reinterpret_cast<const float4*>(&st.km[p][2][16 * tl + 4 * grp]);
-        const float kak[4] = {f1.x, f1.y, f1.z, f1.w};
-        const float kmk[4] = {f2.x, f2.y, f2.z, f2.w};
-#pragma unroll
-        for (int i = 0; i < 4; ++i) s4[i] = fmaf(rq[p], kmk[i], fmaf(mq[p], kak[i], s4[i]));
-      }
-#endif
 #pragma unroll
       for (int p = 0; p < P; ++p) {
         const opT ka = OP::lds(&st.k[tt][p * PI + grp * KSL]);
         const v4i acc = OP::mfma(ka, qop[p], v4i{0, 0, 0, 0});
-#if HACK_PREFILL_SCALE_MFMA
-        const float ask = grp == 0 ? st.km[p][0][tt] : 0.0f;  // s_k
-        const v4f sqk = mfma_f32(ask, bscale[p], v4f{0.0f, 0.0f, 0.0f, 0.0f});
-#pragma unroll
-        for (int i = 0; i < 4; ++i) s4[i] = fmaf(sqk[i], (float)acc[i], s4[i]);  // s_q s_k C~
-#else
         const float4 fk = *reinterpret_cast<const float4*>(&st.km[p][0][16 * tl + 4 * grp]);
         const float ksk[4] = {fk.x, fk.y, fk.z, fk.w};
 #pragma unroll
         for (int i = 0; i < 4; ++i) s4[i] = fmaf(sq[p] * ksk[i], (float)acc[i], s4[i]);  // s_q s_k C~
-#endif
       }
       if (need_mask) {
 #pragma unroll
@@ -559,9 +520,6 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
       // sum of the signed codes of this row's block: all-ones A operand
       const v4i z = OP::mfma(OP::ones(), pop, v4i{0, 0, 0, 0});
       const float pz = ps * (float)z[0];       // s_p * sum p~'
-      // row-side operands: rank terms (s_p sum p~', m~_p) in slots 0, 1; s_p in slot 0
-      const float bpr = grp == 0 ? pz : (grp == 1 ? pm : 0.0f);
-      const float bps = grp == 0 ? ps : 0.0f;
 
       // ---------------- O^T += V'^T P'^T with Eq. 4 (lane: row, channels 16 j + 4 grp + i) ----------------
 #pragma unroll
@@ -570,33 +528,11 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
         const opT va = OP::lds(&st.v[cc][grp * KSL]);
         const v4i acc = OP::mfma(va, pop, v4i{0, 0, 0, 0});
         // (s_p sum p~') m_v + m~_p (s_v sum v' + n m_v), then s_p s_v D~
-#if HACK_PREFILL_PV_RANK_PAIRED
-#elif HACK_PREFILL_PV_RANK_MFMA
-        const float avr = grp == 0 ? vmc[1][cc] : (grp == 1 ? vmc[2][cc] : 0.0f);
-        o[j] = mfma_f32(avr, bpr, o[j]);
-#else
-        {
-          const float4 fm = *reinterpret_cast<const float4*>(&vmc[1][16 * j + 4 * grp]);
-          const float4 fb = *reinterpret_cast<const float4*>(&vmc[2][16 * j + 4 * grp]);
-          const float vmn[4] = {fm.x, fm.y, fm.z, fm.w};
-          const float vbar[4] = {fb.x, fb.y, fb.z, fb.w};
-#pragma unroll
-          for (int i = 0; i < 4; ++i) o[j][i] = fmaf(pm, vbar[i], fmaf(pz, vmn[i], o[j][i]));
-        }
-#endif
-#if HACK_PREFILL_SCALE_MFMA
-        const float avs = grp == 0 ? vmc[0][cc] : 0.0f;
-        const v4f spv = mfma_f32(avs, bps, v4f{0.0f, 0.0f, 0.0f, 0.0f});
-#pragma unroll
-        for (int i = 0; i < 4; ++i) o[j][i] = fmaf(spv[i], (float)acc[i], o[j][i]);
-#else
         const float4 fs = *reinterpret_cast<const float4*>(&vmc[0][16 * j + 4 * grp]);
         const float vs[4] = {fs.x, fs.y, fs.z, fs.w};
 #pragma unroll
         for (int i = 0; i < 4; ++i) o[j][i] = fmaf(ps * vs[i], (float)acc[i], o[j][i]);
-#endif
       }
-#if HACK_PREFILL_PV_RANK_PAIRED
       if (rk_blk < 0) {
         rk_pz = pz;
         rk_pm = pm;
@@ -604,11 +540,8 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
       } else {
         rank_pair(vmc, pz, pm, true);
       }
-#endif
     } else {
-#if HACK_PREFILL_PV_RANK_PAIRED
       if (rk_blk >= 0) rank_pair(vmc, 0.0f, 0.0f, false);
-#endif
       // fp16 open block: O[row][ch] += sum_{t < T} p[row][t] v_t[ch] with unquantized p;
       // p[row][t] lives in lane (row, group (t mod 16) / 4) and is read by a lane shuffle
       const __half* vt = c.v_tail + (((int64_t)s * c.kv_heads + hkv) * PI) * D;
@@ -641,9 +574,7 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4))) voi
   for (int kb = 0; kb < nq; ++kb) block(kb, std::false_type{});
   if (nblk > nq) block(nq, std::true_type{});
 
-#if HACK_PREFILL_PV_RANK_PAIRED
   if (rk_blk >= 0) rank_pair(vm_ring[0], 0.0f, 0.0f, false);
-#endif
   // ---- normalize and write O[row][16 j + 4 grp + i] ----
   const float lsum = xg_sum(l_run);
   if (head_ok && row < L) {

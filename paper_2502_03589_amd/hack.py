@@ -13,8 +13,8 @@ from typing import Optional
 
 import torch
 
-# HACK_LIBRARY may point at another build of the library (e.g. a tuning variant)
-_LIB_PATH = os.environ.get("HACK_LIBRARY") or os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhack.so")
+# the in-tree build only (paper_2502_03589_amd.build writes it here)
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhack.so")
 _lib = None
 
 HACK_OK = 0

@@ -122,7 +122,32 @@ def test_attend_decode_deterministic_and_workspace_reusable():
     torch.cuda.synchronize()
     for o in outs[1:]:
         assert torch.equal(o, outs[0])
-    assert int(ws[-256:].abs().sum()) == 0 or True  # counters live at the end; reuse is checked by equality
+    # the chunk counters (one int32 per (sequence, kv head, four-head group), at the
+    # workspace's start) are back to zero after every call
+    n_counters = case.batch * case.H * ((case.G + 3) // 4)
+    assert int(ws[:4 * n_counters].count_nonzero()) == 0
+
+
+def test_workspace_reused_with_a_shorter_max_len():
+    """One workspace, first a call over 4096 tokens and then one over 1024 (other
+    sequences of the same batch and heads, hence another split count): the second call's
+    counters must not land on the first call's chunk records, so it returns what a
+    fresh workspace returns."""
+    gu = _gpu()
+    from paper_2502_03589_amd import hack as hk
+    gu.announce("workspace reuse 4096 -> 1024")
+    long_ = gu.Case(4343, 4, 2, [4096, 4000, 3900, 4096], 2, 32, group=4).quantize()
+    short = gu.Case(4344, 4, 2, [1024, 1000, 700, 1024], 2, 32, group=4).quantize()
+    ws = hk.decode_workspace(long_.layout, 4, long_.Hq, 4096)
+    q_long = torch.from_numpy(long_.q).to(gu.DEV)
+    q_short = torch.from_numpy(short.q).to(gu.DEV)
+    hk.hack_attend_decode(long_.layout, long_.cache, q_long, long_.lens_dev, 4096, workspace=ws)
+    reused = hk.hack_attend_decode(short.layout, short.cache, q_short, short.lens_dev, 1024, workspace=ws).clone()
+    fresh_ws = hk.decode_workspace(short.layout, 4, short.Hq, 1024)
+    fresh = hk.hack_attend_decode(short.layout, short.cache, q_short, short.lens_dev, 1024, workspace=fresh_ws)
+    torch.cuda.synchronize()
+    assert torch.equal(reused, fresh)
+    assert gu.rel_err(fresh.cpu().numpy(), O.attend_decode(short.q, short.oracle_seqs(), 2)) <= TOL
 
 
 def test_full_size_llama8b_decode_sampled():
@@ -231,6 +256,62 @@ def test_decode_step_equals_append_then_decode(bits, group, H, lens, tail_mode, 
     ref = O.attend_decode(synth_q(a, steps - 1), seqs, H, 8, tail_mode)
     err = gu.rel_err(got.cpu().numpy(), ref)
     print(f"max|d|/|O|inf vs oracle after {steps} steps = {err:.3e}")
+    assert err <= TOL
+
+
+def test_decode_step_dequant_group8_large_grid():
+    """The requantizing open block (DEQUANT) with kv groups of 8 query heads, which the
+    attention splits over two workgroups per chunk, on a grid of more workgroups than
+    the GPU holds at once: batch 64, 8 kv heads, lengths of 1000-2000 tokens, 5 steps,
+    half of the sequences closing a block during them.  Every cache byte must equal the
+    oracle's chain of requantizing appends, and the outputs the oracle's attention."""
+    gu = _gpu()
+    from paper_2502_03589_amd import hack as hk
+    B, H, G, bits, pi, steps = 64, 8, 8, 2, 32, 5
+    g = np.random.default_rng(2468)
+    lens = g.integers(1000, 2001, size=B)
+    lens[::2] = lens[::2] // pi * pi + pi - 2  # T = 30: the block closes at the second step
+    lens = [int(x) for x in lens]
+    gu.announce(f"decode step DEQUANT G=8 B={B} H={H} lens 1000-2000 steps={steps}")
+    case = gu.Case(2469, B, H, lens, bits, pi, group=G, spare_tokens=steps).quantize()
+    # at least one workgroup per (sequence, kv head, four-head group): 1024 of them,
+    # against 256 compute units x 3 resident four-wave workgroups
+    assert B * H * 2 > 256 * 3
+    lens_in = case.lens_dev.clone()
+    lens_out = torch.zeros_like(lens_in)
+    ws = hk.decode_workspace(case.layout, B, case.Hq, case.max_len + steps)
+    for step in range(steps):
+        cur = lens_in.cpu().numpy()
+        kn = torch.from_numpy(np.stack([case.k[s, :, cur[s]] for s in range(B)])).to(gu.DEV)
+        vn = torch.from_numpy(np.stack([case.v[s, :, cur[s]] for s in range(B)])).to(gu.DEV)
+        q = torch.from_numpy(synth_q(case, step)).to(gu.DEV)
+        got = hk.hack_decode_step(case.layout, case.cache, kn, vn, q, lens_in, lens_out, int(cur.max()),
+                                  O.TAIL_DEQUANT, workspace=ws)
+        lens_in, lens_out = lens_out, lens_in
+    torch.cuda.synchronize()
+    final = lens_in.cpu().numpy()
+    assert np.array_equal(final, np.asarray(lens) + steps)
+    seqs = [[None] * H for _ in range(B)]
+    for s_, L0 in enumerate(lens):
+        for h in range(H):
+            sq = O.quantize_sequence(case.k[s_, h, :L0], case.v[s_, h, :L0], bits, pi)
+            for t in range(L0, L0 + steps):
+                sq = O.append_requantizing(sq, case.k[s_, h, t], case.v[s_, h, t], bits)
+            seqs[s_][h] = sq
+    case.lens = final
+    raw = gu.as_sections(case.sections(), case)
+    ref = case.oracle_bytes(seqs)
+    km, vm, tm = gu.valid_masks(case, include_open_block=True)
+    for name, mask in (("k_codes", km), ("k_meta", km), ("k_sums", km), ("v_codes", vm), ("v_meta", vm),
+                       ("v_sums", vm), ("v_tail", tm)):
+        assert np.array_equal(raw[name][mask], ref[name][mask]), name
+    rows = [(b, hq) for b in range(0, B, 2) for hq in range(0, H * G, 4)]
+    want = O.attend_decode(synth_q(case, steps - 1), seqs, H, 8, O.TAIL_DEQUANT, rows=rows)
+    out = got.cpu().numpy()
+    got_rows = np.stack([out[b, hq] for b, hq in rows])
+    want_rows = np.stack([want[b, hq] for b, hq in rows])
+    err = float(np.abs(got_rows - want_rows).max() / np.abs(want_rows).max())
+    print(f"sampled rows max|d|/|O|inf = {err:.3e}")
     assert err <= TOL
 
 

@@ -324,6 +324,41 @@ def test_qp_index_layout_and_distinctness():
     assert len(seen) == 3 * 4 * 3 * 300
 
 
+def test_element_index_layout_and_distinctness():
+    """Stored K/V elements (reading R4): ((seq*H_kv + head) * 2^32 + token) * d + channel.
+    The closed form, and distinct values over a small grid of (seq, head, token,
+    channel) by brute force, so no two stored elements share a threshold."""
+    assert int(O.element_index(1, 4, 2, 3, 5, 128)) == ((1 * 4 + 2) * 2 ** 32 + 3) * 128 + 5
+    seen = set()
+    for b in range(3):
+        for h in range(4):
+            idx = O.element_index(b, 4, h, np.arange(50)[:, None], np.arange(128)[None, :], 128)
+            seen.update(int(x) for x in idx.ravel())
+    assert len(seen) == 3 * 4 * 50 * 128
+
+
+def test_stochastic_sequence_draws_each_elements_own_threshold():
+    """quantize_sequence under stochastic rounding gives K partition (t, p) and V block
+    (blk, channel c) the thresholds of their own elements: the codes equal a direct
+    quantize_partition call with u taken at those elements' indices (a swapped token and
+    channel, or the wrong stream, changes them)."""
+    L, d, pi, bits, seed, seq, head, H = 70, 128, 32, 2, 9, 2, 1, 3
+    k, v = _f16(31, (L, d)), _f16(32, (L, d))
+    sq = O.quantize_sequence(k, v, bits, pi, O.STOCHASTIC, seed, seq, head, H)
+    near = O.quantize_sequence(k, v, bits, pi)
+    assert not np.array_equal(sq.k_codes, near.k_codes)
+    for t, p in ((0, 0), (5, 3), (69, 2)):
+        ch = np.arange(p * pi, (p + 1) * pi)
+        u = O.stochastic_threshold(seed, O.STREAM_K, O.element_index(seq, H, head, t, ch, d))
+        c, m, s, tot = O.quantize_partition(k[t, ch][None, :], bits, "f16", O.STOCHASTIC, u[None, :])
+        assert np.array_equal(sq.k_codes[t, ch], c[0]) and sq.k_sum[t, p] == tot[0]
+    for blk, c_ in ((0, 0), (1, 77), (1, 127)):
+        toks = np.arange(blk * pi, (blk + 1) * pi)
+        u = O.stochastic_threshold(seed, O.STREAM_V, O.element_index(seq, H, head, toks, c_, d))
+        c, m, s, tot = O.quantize_partition(v[toks, c_][None, :], bits, "f16", O.STOCHASTIC, u[None, :])
+        assert np.array_equal(sq.v_codes[blk, :, c_], c[0]) and sq.v_sum[blk, c_] == tot[0]
+
+
 def test_stochastic_query_codes_are_floor_or_ceil_and_unbiased():
     """Over 4000 seeds each Q code is floor(t) or floor(t)+1 with t = (x-m)*fl(1/s) in
     float32 (R3), and the mean dequantized value s*c + m approaches x (E[c] = t)."""
