@@ -211,16 +211,16 @@ def test_partition128_workspace_follows_its_plan(lib):
     """Partition 128 chunks sequences into whole 512-token spans (one 128-token block
     per wave) so that the grid holds 4 (2-bit) or 2 (4-bit) workgroups per compute
     unit of 256: at decode_llama8b_l4096's shapes that is 8 (2-bit) or 4 (4-bit)
-    chunks per sequence; records of 4 + 128 floats per (sequence, kv head, chunk,
-    query head) come first, 256-byte aligned, then one counter per (sequence, kv head,
-    group of four query heads)."""
+    chunks per sequence; one int32 counter per (sequence, kv head, group of four query
+    heads) comes first, 256-byte aligned, then records of 4 + 128 floats per (sequence,
+    kv head, chunk, query head)."""
     def expect(B, H, G, L, per_cu):
         span, pairs, nhg = 512, B * H, (G + 3) // 4
         spans_seq = -(-L // span)
         wg = min(max(-(-(spans_seq * pairs * nhg) // (256 * per_cu)), 1), 64)
         splits = -(-L // (wg * span))
         rec = -(-(pairs * splits * G * (4 + 128) * 4) // 256) * 256
-        return rec + -(-(pairs * nhg * 4) // 256) * 256, splits
+        return -(-(pairs * nhg * 4) // 256) * 256 + rec, splits
     for bits, per_cu in ((2, 4), (4, 2)):
         lay = hk.hack_kv_layout_make(128, 8, bits, 128, 4096)
         ws, splits = expect(16, 8, 4, 4096, per_cu)
