@@ -14,6 +14,8 @@ What it computes (citations are to the paper):
     with Q quantized to 8 bits, K/V to b bits along the contraction
     dimension, P quantized to 8 bits per V block, and both products done by
     Eq. 4 using the cached code sums                       (Sec. 5.3, summation elimination)
+  * QKV generation Q = E W_Q, K = E W_K, V = E W_V from the prompt's embeddings
+    (Sec. 4, Eq. 1), in float64 rounded to fp16, in front of the quantizer
   * the open (last, partial) block of V kept in fp16 and multiplied
     unquantized (requantization elimination, Sec. 5.3), or re-quantized from its
     fp16 originals with n = T elements (the re-quantizing alternative).
@@ -522,6 +524,51 @@ def prefill_row(q, sq: SeqKV, i: int, causal: bool, qp_bits: int = 8, sr: Option
     prob = np.zeros(L)
     prob[:upto] = softmax(S)
     return pv_blocks(prob, sq, qp_bits, TAIL_FP16, sr)
+
+
+# ----------------------------------------------------------------------------
+# QKV generation in front of prefill attention (Sec. 4, Eq. 1; fused with
+# quantization and attention in the paper's prefill kernel, Sec. 6)
+# ----------------------------------------------------------------------------
+def project_qkv(E, W, q_heads: int, kv_heads: int, head_dim: int, tokens=None):
+    """Eq. 1: Q^h = E W_Q^h, K^h = E W_K^h, V^h = E W_V^h for one sequence.
+
+    E: fp16 [L][hidden], the prompt's embeddings.  W: fp16 [(H_q + 2 H_kv) * d][hidden],
+    one row per output channel: the H_q query heads' d channels, then the H_kv key
+    heads', then the H_kv value heads' (the transposes of W_Q, W_K, W_V side by side).
+    The products are summed in float64 and rounded once to fp16, the precision of the
+    K/V values the quantizer takes (and of the Q the attention takes).  `tokens`
+    optionally restricts the rows (a list of token indices).
+    Returns fp16 Q [H_q][n][d], K [H_kv][n][d], V [H_kv][n][d]."""
+    E = np.asarray(E, np.float16)
+    W = np.asarray(W, np.float16)
+    if tokens is not None:
+        E = E[np.asarray(tokens)]
+    n = E.shape[0]
+    d = head_dim
+    out = (E.astype(np.float64) @ W.astype(np.float64).T).astype(np.float16)   # [n][N]
+    heads = out.reshape(n, q_heads + 2 * kv_heads, d).transpose(1, 0, 2)
+    return (np.ascontiguousarray(heads[:q_heads]), np.ascontiguousarray(heads[q_heads:q_heads + kv_heads]),
+            np.ascontiguousarray(heads[q_heads + kv_heads:]))
+
+
+def prefill_from_embeddings(E, W, q_heads: int, kv_heads: int, head_dim: int, bits: int, partition: int,
+                            causal: bool = True, qp_bits: int = 8, rows=None, rounding: int = NEAREST_EVEN,
+                            seed: int = 0):
+    """The paper's prefill (Sec. 6): QKV generation (Eq. 1), quantization of K and V
+    (Sec. 5.2-5.3) and attention with homomorphic quantization, for a batch.
+    E: fp16 [B][L][hidden].  Returns (O float32 [B][H_q][L][d], Q fp16 [B][H_q][L][d],
+    seqs[b][h] SeqKV).  `rows` restricts the attention to (b, h_q, i) triples."""
+    E = np.asarray(E, np.float16)
+    B = E.shape[0]
+    Qs, seqs = [], []
+    for b in range(B):
+        Q, K, V = project_qkv(E[b], W, q_heads, kv_heads, head_dim)
+        Qs.append(Q)
+        seqs.append([quantize_sequence(K[h], V[h], bits, partition, rounding, seed, b, h, kv_heads)
+                     for h in range(kv_heads)])
+    Q = np.stack(Qs)
+    return attend_prefill(Q, seqs, kv_heads, causal, qp_bits, rows), Q, seqs
 
 
 def attend_decode(q, seqs, kv_heads: int, qp_bits: int = 8, tail_mode: int = TAIL_FP16, rows=None,
