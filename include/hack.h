@@ -200,6 +200,24 @@ hack_status hack_attend_decode(const hack_kv_layout* layout, const hack_kv_cache
                                int32_t batch, int32_t max_len, int32_t tail_mode, float* out_dev,
                                void* workspace_dev, int64_t workspace_bytes, hipStream_t stream);
 
+/* hack_attend_decode without a caller workspace, for callers that cannot allocate
+ * device memory or pass a scratch buffer: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc.  Arguments and results as hack_attend_decode;
+ * the split-K counters and chunk records live in a library-owned static device array
+ * instead (one per GPU, 16.25 MiB, held until the process ends).  Limits: at most
+ * 65536 chunk counters (batch * H_kv * ceil(H_q/H_kv / 4)) and 16 MiB of chunk records
+ * (hack_decode_workspace_bytes(...) minus its counter bytes); larger shapes return
+ * HACK_ERR_WORKSPACE before anything is launched.  Nothing is allocated: no hipMalloc,
+ * hipFree or allocating library call.  The first call on a device looks the array up
+ * and launches a small kernel on `stream` that clears its counters; every call leaves
+ * them zero again.  All calls on one GPU share the array, so calls that may overlap
+ * on one GPU (several streams or host threads without ordering between them) race and
+ * give wrong results.  HACK_ERR_HIP if the array cannot be located. */
+hack_status hack_attend_decode_noalloc(const hack_kv_layout* layout, const hack_kv_cache* cache,
+                                       const void* q_dev, int32_t num_q_heads,
+                                       const int32_t* seq_lens_dev, int32_t batch, int32_t max_len,
+                                       int32_t tail_mode, float* out_dev, hipStream_t stream);
+
 /* One decode step (Sec. 5.3 with L_Q = 1, and the decode-side quantize-on-write of
  * §6, fused in one launch): for every sequence s and kv head, the new token
  * (k_new_dev / v_new_dev: fp16 [batch][H_kv][head_dim]) is written as token

@@ -1,8 +1,24 @@
 // C ABI of the library: argument validation on the host, then kernel launches
 // on the caller's stream.  Nothing here allocates device memory or synchronizes.
 #include <cstring>
+#include <mutex>
 
 #include "hack_internal.hpp"
+
+// Split-K workspace of hack_attend_decode_noalloc: one copy per GPU, held until the
+// process ends.  Layout as a caller's workspace (hack::DecodePlan): chunk counters
+// from offset 0 (at most kScratchCounters of them), chunk records from
+// kScratchCounterBytes (at most kScratchRecordBytes).  Static storage is zero-filled
+// when the code object is loaded, so the counters start at zero; every call leaves
+// them zero.  In host code `scratch` is only a handle for hipGetSymbolAddress: its
+// device address is looked up per device and kept in g_scratch_ptr.
+namespace {
+constexpr int64_t kScratchCounters = 65536;
+constexpr int64_t kScratchCounterBytes = kScratchCounters * 4;
+constexpr int64_t kScratchRecordBytes = 16ll << 20;
+constexpr int64_t kScratchBytes = kScratchCounterBytes + kScratchRecordBytes;
+}  // namespace
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
 
 using hack::CacheView;
 
@@ -93,6 +109,33 @@ void bind_workspace(hack::DecodeArgs& a, const hack::DecodePlan& plan, void* ws)
 hipError_t launch_attend(const hack_kv_layout& l, const hack::DecodeArgs& a, int batch, hipStream_t stream) {
   if (l.partition == 128) return hack::launch_decode128(l, a, batch, stream);
   return hack::launch_decode(l, a, batch, hack::MODE_ATTEND, stream);
+}
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];  // device address of `scratch` per device; guarded by g_scratch_mu
+
+__global__ void zero_words_kernel(int32_t* p, int64_t n) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = 0;
+}
+
+// Device address of the current device's `scratch`.  The first call on a device looks
+// it up and clears its counters with a kernel on `stream` (a kernel rather than a
+// memset, so that a caller may capture it in a graph).  Returns nullptr on failure.
+void* scratch_for_current_device(hipStream_t stream) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return nullptr;
+    hipLaunchKernelGGL(zero_words_kernel, dim3(64), dim3(256), 0, stream, static_cast<int32_t*>(p),
+                       kScratchCounters);
+    if (hipGetLastError() != hipSuccess) return nullptr;
+    g_scratch_ptr[dev] = p;
+  }
+  return g_scratch_ptr[dev];
 }
 
 }  // namespace
@@ -228,6 +271,31 @@ hack_status hack_attend_decode(const hack_kv_layout* layout, const hack_kv_cache
   bind_workspace(a, plan, workspace_dev);
   a.tail_requant = tail_mode;  // 0: fp16 open block; 1, 2: its codes (re-quantized on append)
   (void)hipGetLastError();
+  return from_hip(launch_attend(*layout, a, batch, stream));
+}
+
+hack_status hack_attend_decode_noalloc(const hack_kv_layout* layout, const hack_kv_cache* cache, const void* q_dev,
+                                       int32_t num_q_heads, const int32_t* seq_lens_dev, int32_t batch,
+                                       int32_t max_len, int32_t tail_mode, float* out_dev, hipStream_t stream) {
+  hack::DecodeArgs a;
+  int64_t cap = 0;
+  hack_status st = decode_common(layout, cache, q_dev, num_q_heads, seq_lens_dev, batch, max_len, a, &cap);
+  if (st != HACK_OK) return st;
+  if (!out_dev || !(tail_mode == HACK_TAIL_FP16 || tail_mode == HACK_TAIL_REQUANT || tail_mode == HACK_TAIL_DEQUANT))
+    return HACK_ERR_INVALID_ARGUMENT;
+  const hack::DecodePlan plan = plan_attend(*layout, batch, num_q_heads, max_len);
+  if (plan.counter_bytes > kScratchCounterBytes || plan.workspace_bytes - plan.record_offset > kScratchRecordBytes)
+    return HACK_ERR_WORKSPACE;
+  if (batch == 0) return HACK_OK;
+  (void)hipGetLastError();
+  uint8_t* ws = static_cast<uint8_t*>(scratch_for_current_device(stream));
+  if (!ws) return HACK_ERR_HIP;
+  a.out = out_dev;
+  a.counters = reinterpret_cast<int32_t*>(ws);
+  a.partials = reinterpret_cast<float*>(ws + kScratchCounterBytes);
+  a.chunk = plan.chunk;
+  a.splits = plan.splits;
+  a.tail_requant = tail_mode;
   return from_hip(launch_attend(*layout, a, batch, stream));
 }
 

@@ -62,6 +62,7 @@ _SIGS = {
     "hack_append": (_I32, [_LAY, _CAC, _P, _P, _P, _I32, _I32, _I32, _P]),
     "hack_decode_workspace_bytes": (_I64, [_LAY, _I32, _I32, _I32]),
     "hack_attend_decode": (_I32, [_LAY, _CAC, _P, _I32, _P, _I32, _I32, _I32, _P, _P, _I64, _P]),
+    "hack_attend_decode_noalloc": (_I32, [_LAY, _CAC, _P, _I32, _P, _I32, _I32, _I32, _P, _P]),
     "hack_decode_step": (_I32, [_LAY, _CAC, _P, _P, _P, _I32, _P, _P, _I32, _I32, _I32, _P, _P, _I64, _P]),
     "hack_attend_prefill": (_I32, [_LAY, _CAC, _P, _I32, _I32, _I32, _I32, _P, _P]),
     "hack_status_string": (ctypes.c_char_p, [_I32]),
@@ -231,6 +232,20 @@ def hack_attend_decode(layout, cache: KVCache, q: torch.Tensor, seq_lens: torch.
                                     hq, _dev(seq_lens, torch.int32, "seq_lens"), batch, max_len, tail_mode,
                                     _dev(out, torch.float32, "out"), _dev(workspace, torch.uint8, "workspace"),
                                     workspace.numel(), _stream(stream)), "hack_attend_decode")
+    return out
+
+
+def hack_attend_decode_noalloc(layout, cache: KVCache, q: torch.Tensor, seq_lens: torch.Tensor, max_len: int,
+                               tail_mode: int = TAIL_FP16, out: Optional[torch.Tensor] = None,
+                               stream=None) -> torch.Tensor:
+    """hack_attend_decode with the library's own static split-K scratch (no workspace)."""
+    batch, hq, d = q.shape
+    if out is None:
+        out = torch.empty((batch, hq, d), dtype=torch.float32, device=q.device)
+    _check(lib().hack_attend_decode_noalloc(ctypes.byref(layout), ctypes.byref(cache.struct),
+                                            _dev(q, torch.float16, "q"), hq, _dev(seq_lens, torch.int32, "seq_lens"),
+                                            batch, max_len, tail_mode, _dev(out, torch.float32, "out"),
+                                            _stream(stream)), "hack_attend_decode_noalloc")
     return out
 
 

@@ -229,3 +229,26 @@ def test_partition128_workspace_follows_its_plan(lib):
         for B, H, G, L in ((1, 1, 1, 1), (3, 2, 8, 5000), (1, 8, 6, 131072), (64, 8, 4, 300)):
             lay = hk.hack_kv_layout_make(128, H, bits, 128, 512)
             assert hk.hack_decode_workspace_bytes(lay, B, H * G, L) == expect(B, H, G, L, per_cu)[0]
+
+
+def test_noalloc_limits_checked_before_launch(lib):
+    """hack_attend_decode_noalloc takes its split-K state from a static scratch of 65536
+    counters and 16 MiB of chunk records: larger shapes get HACK_ERR_WORKSPACE on the
+    host, other argument errors the same statuses as hack_attend_decode, and a batch of
+    0 succeeds, all before anything touches the device."""
+    lay = hk.hack_kv_layout_make(128, 8, 2, 32, 256)
+    L = ctypes.byref(lay)
+    paged = _Fake(pages=4, table=True, mbps=512)  # capacity 131072 tokens per sequence
+    C = ctypes.byref(paged.struct)
+    p = ctypes.c_void_p(0x5000)
+    # 8192 sequences x 8 kv heads x 2 four-head groups = 131072 counters
+    assert lib.hack_attend_decode_noalloc(L, C, p, 64, p, 8192, 1024, 0, p, None) == 4
+    # 64 sequences of 131072 tokens, group 8: chunk records beyond 16 MiB
+    full = hk.hack_decode_workspace_bytes(lay, 64, 64, 131072)
+    assert full - 256 * ((64 * 8 * 2 * 4 + 255) // 256) > 16 << 20
+    assert lib.hack_attend_decode_noalloc(L, C, p, 64, p, 64, 131072, 0, p, None) == 4
+    assert lib.hack_attend_decode_noalloc(L, C, p, 7, p, 2, 100, 0, p, None) == 1       # H_q % H_kv
+    assert lib.hack_attend_decode_noalloc(L, C, p, 16, p, 2, 100, 5, p, None) == 1      # tail mode
+    assert lib.hack_attend_decode_noalloc(L, C, p, 16, p, 2, 100, 0, None, None) == 1   # no output
+    assert lib.hack_attend_decode_noalloc(L, C, p, 16, p, 2, 131073, 0, p, None) == 3   # capacity
+    assert lib.hack_attend_decode_noalloc(L, C, p, 16, p, 0, 100, 0, p, None) == 0
