@@ -105,7 +105,7 @@ def parse():
                     default=None,
                     help="time another decode workload instead (one JSON line per configuration; "
                          "not the headline line)")
-    ap.add_argument("--only", choices=["decode", "llama8b", "long", "prefill", "copy", "cpu"], default=None,
+    ap.add_argument("--only", choices=["decode", "llama8b", "long", "prefill", "project", "copy", "cpu"], default=None,
                     help="profiling aid: run one leg alone (decode = the headline 70B-share decode step; "
                          "copy = plain device copy of a known size, the calibration for HBM byte counters)")
     return ap.parse_args()
@@ -182,7 +182,7 @@ def _oracle_worker(pairs, barrier, results, slot):
     return nbytes, dt
 
 
-def cpu_baseline_decode(pairs_per_core: int = 6):
+def cpu_baseline_decode(pairs_per_core: int = 10):
     """The oracle on every host core: one forked worker per core, each timing the
     decode attention of `pairs_per_core` whole (sequence, kv head) pairs of the headline
     workload (lengths from the same seeded draw); aggregate rate = all bytes / the
@@ -448,6 +448,7 @@ def main():
     cpu = None
     if not args.no_cpu_baseline and args.only in (None, "cpu"):
         cpu = cpu_baseline_decode()
+        print(f"[bench] oracle baseline: {cpu.get('value')} GB/s on {cpu.get('cores')} cores", file=sys.stderr, flush=True)
         if args.only == "cpu":
             print(json.dumps({"cpu_baseline": cpu}), flush=True)
             return
@@ -460,6 +461,9 @@ def main():
     if args.only == "prefill":
         print(json.dumps({"prefill": bench_prefill(args.prefill_iters)}), flush=True)
         return
+    if args.only == "project":
+        print(json.dumps({"prefill_from_embeddings": bench_prefill_embeddings(args.prefill_iters)}), flush=True)
+        return
     if args.only == "llama8b":
         print(json.dumps({"decode_llama8b_l4096": bench_llama8b(args.steps, args.warmup, args.replicas)[0]}), flush=True)
         return
@@ -469,7 +473,11 @@ def main():
     import torch
     torch.cuda.set_device(torch.device("cuda:0"))
 
+    def progress(msg):
+        print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
     step_bytes, ms_per_step, cfg, roof = bench_ragged(args.steps, args.warmup)
+    progress(f"decode_70b_ragged: {ms_per_step:.4f} ms per step")
     result = {
         "metric": "decode: compressed-KV GB/s (append + attend per step)",
         "value": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 2),
@@ -488,7 +496,9 @@ def main():
     }
     if args.only is None:
         result["decode_llama8b_l4096"], result["quantize"] = bench_llama8b(args.steps, args.warmup, args.replicas)
+        progress("decode_llama8b_l4096 done")
         result["decode_long_l131072"] = bench_long()
+        progress("decode_long_l131072 done")
         result["decode_tiny_l256"] = bench_tiny()
         result["box_copy_GBs"] = round(copy_bandwidth(), 1)
         if not args.no_prefill:
@@ -497,6 +507,8 @@ def main():
             result["prefill_qp4"] = bench_prefill(max(3, args.prefill_iters // 2), 4)
             # the paper's rounding: stochastic K/V, Q and P codes
             result["prefill_stochastic"] = bench_prefill(max(3, args.prefill_iters // 2), 8, 1)
+            result["prefill_from_embeddings"] = bench_prefill_embeddings(max(3, args.prefill_iters // 2))
+            progress("prefill done")
         if cpu is not None:
             result["cpu_baseline"] = cpu
     print(json.dumps(result), flush=True)
@@ -548,6 +560,50 @@ def bench_prefill(iters: int, qp_bits: int = 8, rounding: int = 0):
             "roofline": {"bound": "mfma", "kernel": "prefill_kernel", "achieved": round(tops, 2),
                          "peak": INT8_PEAK_TOPS, "unit": "TOPS (int8)", "frac": round(tops / INT8_PEAK_TOPS, 4),
                          "traffic": None}}
+
+
+def bench_prefill_embeddings(iters: int):
+    """The prefill from embeddings at the prefill workload's shapes with a
+    Llama-3-8B-sized hidden dimension (batch 1, 8192 tokens, 32/8 heads, hidden 4096,
+    4-bit K/V, partition 64): the fused QKV projection + quantize-on-write kernel, then
+    the attention.  The projection's work is 2 x tokens x hidden x (H_q + 2 H_kv) x 128
+    fp16 operations on the matrix cores."""
+    import torch
+    from paper_2502_03589_amd import hack as hk
+    from paper_2502_03589_amd import synth
+    wl = synth.WORKLOADS["prefill_l8192"]
+    B, Hq, H, d, L, hidden = wl.batch, wl.q_heads, wl.kv_heads, wl.head_dim, wl.context, 4096
+    N = (Hq + 2 * H) * d
+    dev = torch.device("cuda:0")
+    lay = hk.hack_kv_layout_make(d, H, wl.kv_bits, wl.partition, L, 8, 0, wl.seed)
+    c = hk.KVCache(lay, B, B, None, dev)
+    e = torch.from_numpy(synth.normal_f16(wl.seed, "misc", (B, L, hidden), sub=1)).to(dev)
+    w = torch.from_numpy((synth.normal_f16(wl.seed, "misc", (N, hidden), sub=2).astype(np.float32)
+                          / np.sqrt(hidden)).astype(np.float16)).to(dev)
+    q = torch.empty((B, Hq, L, d), dtype=torch.float16, device=dev)
+    out = torch.empty((B, Hq, L, d), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+    hk.hack_prefill_from_embeddings(lay, c, e, w, Hq, True, q, out)
+    torch.cuda.synchronize()
+    e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+    pt, at = [], []
+    for _ in range(iters):
+        e0.record(stream)
+        hk.hack_project_qkv(lay, c, e, w, Hq, q)
+        e1.record(stream)
+        hk.hack_attend_prefill(lay, c, q, True, out)
+        e2.record(stream)
+        torch.cuda.synchronize()
+        pt.append(e0.elapsed_time(e1))
+        at.append(e1.elapsed_time(e2))
+    p_ms, a_ms = float(np.median(pt)), float(np.median(at))
+    flops = 2 * B * L * hidden * N
+    tf = flops / (p_ms * 1e-3) / 1e12
+    return {"workload": "prefill_l8192 from embeddings (hidden 4096)", "project_ms": round(p_ms, 4),
+            "attend_ms": round(a_ms, 4), "total_ms": round(p_ms + a_ms, 4), "project_flops": flops,
+            "roofline": {"bound": "mfma", "kernel": "project_kernel (QKV GEMM + quantize-on-write)",
+                         "achieved": round(tf, 2), "peak": 2500.0, "unit": "TFLOP/s (fp16)",
+                         "frac": round(tf / 2500.0, 4), "traffic": None}}
 
 
 def bench_workload(name: str, steps: int, warmup: int):

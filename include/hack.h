@@ -250,6 +250,35 @@ hack_status hack_attend_prefill(const hack_kv_layout* layout, const hack_kv_cach
                                 const void* q_dev, int32_t num_q_heads, int32_t batch, int32_t len,
                                 int32_t causal, float* out_dev, hipStream_t stream);
 
+/* QKV generation fused with quantize-on-write: the front of the prefill (Sec. 4, Eq. 1,
+ * fused as in the paper's prefill kernel, Sec. 6).  For every sequence s and token t <
+ * len: out[n] = sum_i E[s][t][i] W[n][i] over the hidden dimension, accumulated in
+ * fp32 and rounded to fp16, for n over the output channels of the H_q query heads,
+ * then the H_kv key heads, then the H_kv value heads (head_dim 128 channels each).
+ *   e_dev:     fp16 [batch][len][hidden], the prompt's embeddings;
+ *   w_dev:     fp16 [(H_q + 2 H_kv) * 128][hidden], one row per output channel (the
+ *              transposed W_Q, W_K, W_V stacked, as a fused QKV weight);
+ *   q_out_dev: fp16 [batch][H_q][len][128], the query heads, in the layout
+ *              hack_attend_prefill takes.
+ * The key and value heads are not written out: they are quantized into `cache` exactly
+ * as hack_quantize quantizes fp16 K and V of length len (codes, min/scale, sums, the
+ * open V block in fp16 and re-quantized with n = T), with the layout's rounding.
+ * Requires head_dim 128 and hidden a positive multiple of 64 (else HACK_ERR_UNSUPPORTED);
+ * HACK_ERR_CAPACITY if len exceeds the cache's capacity.  One kernel. */
+hack_status hack_project_qkv(const hack_kv_layout* layout, const hack_kv_cache* cache, const void* e_dev,
+                             const void* w_dev, int32_t num_q_heads, int32_t hidden, int32_t batch,
+                             int32_t len, void* q_out_dev, hipStream_t stream);
+
+/* The prefill from embeddings (Sec. 6): hack_project_qkv, then hack_attend_prefill on
+ * its query heads over the cache it wrote (two kernels on `stream`).  q_out_dev is the
+ * caller's fp16 [batch][H_q][len][128] buffer for the query heads; out_dev fp32
+ * [batch][H_q][len][128].  The shape limits of both calls apply and are checked before
+ * anything is launched. */
+hack_status hack_prefill_from_embeddings(const hack_kv_layout* layout, const hack_kv_cache* cache,
+                                         const void* e_dev, const void* w_dev, int32_t num_q_heads,
+                                         int32_t hidden, int32_t batch, int32_t len, int32_t causal,
+                                         void* q_out_dev, float* out_dev, hipStream_t stream);
+
 /* Static, NUL-terminated description of a status code. */
 const char* hack_status_string(hack_status status);
 

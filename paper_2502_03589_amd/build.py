@@ -15,7 +15,7 @@ CSRC = os.path.join(HERE, "csrc")
 OBJ = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libhack.so")
 SOURCES = ["hack_api.hip", "kernels_quant.hip", "kernels_decode.hip", "kernels_decode128.hip",
-           "kernels_prefill.hip"]
+           "kernels_prefill.hip", "kernels_project.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

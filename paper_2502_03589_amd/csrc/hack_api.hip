@@ -371,6 +371,49 @@ hack_status hack_attend_prefill(const hack_kv_layout* layout, const hack_kv_cach
                                        num_q_heads, batch, len, causal != 0, out_dev, stream));
 }
 
+hack_status hack_project_qkv(const hack_kv_layout* layout, const hack_kv_cache* cache, const void* e_dev,
+                             const void* w_dev, int32_t num_q_heads, int32_t hidden, int32_t batch, int32_t len,
+                             void* q_out_dev, hipStream_t stream) {
+  if (!layout_ok(layout) || !e_dev || !w_dev || !q_out_dev || batch < 0 || len < 0 || hidden <= 0)
+    return HACK_ERR_INVALID_ARGUMENT;
+  if (num_q_heads < 1 || num_q_heads % layout->num_kv_heads != 0) return HACK_ERR_INVALID_ARGUMENT;
+  if (layout->head_dim != 128 || hidden % 64 != 0) return HACK_ERR_UNSUPPORTED;
+  const int64_t cap = cache_capacity(layout, cache, batch);
+  if (cap < 0) return HACK_ERR_INVALID_ARGUMENT;
+  if (len > cap) return HACK_ERR_CAPACITY;
+  const int64_t tiles = (int64_t)batch * ((len + 127) / 128) * (num_q_heads + 2 * layout->num_kv_heads);
+  if (tiles > INT32_MAX) return HACK_ERR_UNSUPPORTED;  // one workgroup per tile in a 1-D grid
+  if (batch == 0 || len == 0) return HACK_OK;
+  hack::ProjectArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.c = make_view(layout, cache);
+  a.e = static_cast<const __half*>(e_dev);
+  a.w = static_cast<const __half*>(w_dev);
+  a.q = static_cast<__half*>(q_out_dev);
+  a.batch = batch;
+  a.len = len;
+  a.hidden = hidden;
+  a.q_heads = num_q_heads;
+  a.kv_heads = layout->num_kv_heads;
+  (void)hipGetLastError();
+  return from_hip(hack::launch_project(*layout, a, stream));
+}
+
+hack_status hack_prefill_from_embeddings(const hack_kv_layout* layout, const hack_kv_cache* cache,
+                                         const void* e_dev, const void* w_dev, int32_t num_q_heads, int32_t hidden,
+                                         int32_t batch, int32_t len, int32_t causal, void* q_out_dev,
+                                         float* out_dev, hipStream_t stream) {
+  if (!layout_ok(layout) || !out_dev) return HACK_ERR_INVALID_ARGUMENT;
+  // the attention's own checks first, so that nothing is launched for a shape it rejects
+  if (num_q_heads < 1 || num_q_heads % layout->num_kv_heads != 0) return HACK_ERR_INVALID_ARGUMENT;
+  const hack_status sh = attention_shape(layout, num_q_heads);
+  if (sh != HACK_OK) return sh;
+  if (layout->sum_bytes == 0 || layout->partition == 128 || batch > kMaxGridYZ) return HACK_ERR_UNSUPPORTED;
+  hack_status st = hack_project_qkv(layout, cache, e_dev, w_dev, num_q_heads, hidden, batch, len, q_out_dev, stream);
+  if (st != HACK_OK) return st;
+  return hack_attend_prefill(layout, cache, q_out_dev, num_q_heads, batch, len, causal, out_dev, stream);
+}
+
 const char* hack_status_string(hack_status status) {
   switch (status) {
     case HACK_OK: return "ok";

@@ -92,6 +92,23 @@ hipError_t launch_decode(const hack_kv_layout& lay, const DecodeArgs& a, int bat
 // Decode attention (MODE_ATTEND) for partition 128: VALU int8-dot kernel.
 hipError_t launch_decode128(const hack_kv_layout& lay, const DecodeArgs& a, int batch, hipStream_t stream);
 
+// QKV generation fused with quantize-on-write (kernels_project.hip).
+struct ProjectArgs {
+  CacheView c;
+  const __half* e;    // [batch][len][hidden] embeddings
+  const __half* w;    // [(H_q + 2 H_kv) * 128][hidden] weights, one row per output channel
+  __half* q;          // [batch][H_q][len][128] query heads out
+  int batch, len, hidden, q_heads, kv_heads;
+  // filled by launch_project
+  int mtiles;         // 128-token tiles per sequence
+  int ntiles;         // head tiles: H_q + 2 H_kv
+  int64_t total;      // batch * mtiles * ntiles
+  int stochastic;
+  uint64_t key_k, key_v;
+};
+
+hipError_t launch_project(const hack_kv_layout& lay, const ProjectArgs& a, hipStream_t stream);
+
 hipError_t launch_prefill(const hack_kv_layout& lay, const CacheView& c, const __half* q,
                           int num_q_heads, int batch, int len, int causal, float* out,
                           hipStream_t stream);

@@ -65,6 +65,8 @@ _SIGS = {
     "hack_attend_decode_noalloc": (_I32, [_LAY, _CAC, _P, _I32, _P, _I32, _I32, _I32, _P, _P]),
     "hack_decode_step": (_I32, [_LAY, _CAC, _P, _P, _P, _I32, _P, _P, _I32, _I32, _I32, _P, _P, _I64, _P]),
     "hack_attend_prefill": (_I32, [_LAY, _CAC, _P, _I32, _I32, _I32, _I32, _P, _P]),
+    "hack_project_qkv": (_I32, [_LAY, _CAC, _P, _P, _I32, _I32, _I32, _I32, _P, _P]),
+    "hack_prefill_from_embeddings": (_I32, [_LAY, _CAC, _P, _P, _I32, _I32, _I32, _I32, _I32, _P, _P, _P]),
     "hack_status_string": (ctypes.c_char_p, [_I32]),
     "hack_debug_qk_products": (_I32, [_LAY, _CAC, _P, _I32, _P, _I32, _I32, _P, _P, _P, _P]),
     "hack_debug_pv_products": (_I32, [_LAY, _CAC, _P, _P, _I32, _P, _I32, _I32, _P, _P, _P]),
@@ -278,6 +280,37 @@ def hack_attend_prefill(layout, cache: KVCache, q: torch.Tensor, causal: bool = 
                                      hq, batch, length, int(bool(causal)), _dev(out, torch.float32, "out"),
                                      _stream(stream)), "hack_attend_prefill")
     return out
+
+
+def hack_project_qkv(layout, cache: KVCache, e: torch.Tensor, w: torch.Tensor, num_q_heads: int,
+                     q_out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """QKV generation fused with quantize-on-write: e fp16 [B][L][hidden], w fp16
+    [(H_q + 2 H_kv) * 128][hidden].  Returns the fp16 query heads [B][H_q][L][128];
+    the key and value heads go quantized into `cache`."""
+    batch, length, hidden = e.shape
+    if q_out is None:
+        q_out = torch.empty((batch, num_q_heads, length, 128), dtype=torch.float16, device=e.device)
+    _check(lib().hack_project_qkv(ctypes.byref(layout), ctypes.byref(cache.struct), _dev(e, torch.float16, "e"),
+                                  _dev(w, torch.float16, "w"), num_q_heads, hidden, batch, length,
+                                  _dev(q_out, torch.float16, "q_out"), _stream(stream)), "hack_project_qkv")
+    return q_out
+
+
+def hack_prefill_from_embeddings(layout, cache: KVCache, e: torch.Tensor, w: torch.Tensor, num_q_heads: int,
+                                 causal: bool = True, q_out: Optional[torch.Tensor] = None,
+                                 out: Optional[torch.Tensor] = None, stream=None):
+    """Projection + quantize-on-write + prefill attention; returns (out fp32, q fp16)."""
+    batch, length, hidden = e.shape
+    if q_out is None:
+        q_out = torch.empty((batch, num_q_heads, length, 128), dtype=torch.float16, device=e.device)
+    if out is None:
+        out = torch.empty((batch, num_q_heads, length, 128), dtype=torch.float32, device=e.device)
+    _check(lib().hack_prefill_from_embeddings(ctypes.byref(layout), ctypes.byref(cache.struct),
+                                              _dev(e, torch.float16, "e"), _dev(w, torch.float16, "w"), num_q_heads,
+                                              hidden, batch, length, int(bool(causal)),
+                                              _dev(q_out, torch.float16, "q_out"), _dev(out, torch.float32, "out"),
+                                              _stream(stream)), "hack_prefill_from_embeddings")
+    return out, q_out
 
 
 def hack_debug_qk_products(layout, cache: KVCache, q: torch.Tensor, seq_lens: torch.Tensor, max_len: int,
