@@ -10,18 +10,21 @@
 //         (head h, channel quarter q), block-diagonal so that lane group g only
 //         carries quarter g; B = 2/4-bit K codes unpacked in registers (lane = token,
 //         group = quarter).  Lane (t, g) receives the four quarter products of head g.
-//   Eq. 4 v_mfma_f32_16x16x4_f32 with B = the lane's own K partition metadata
-//         spreads it over the output layout: one product gives s_q s_k per
-//         (head, quarter), two more give the rank-1 terms (m~_q s_k sum k' and
-//         R_q m_k) already summed over the partitions.  The VALU only converts the
-//         integer products and takes four fused multiply-adds per score (log2 units).
+//   Eq. 4 matrix-core products with B = the lane's own K partition metadata spread
+//         it over the output layout: v_mfma_f32_16x16x16_f16 gives s_q s_k per (head,
+//         quarter) from s_q as three fp16 pieces against the stored fp16 s_k (as
+//         exact as fp32, half the issue cycles of the fp32 product), two
+//         v_mfma_f32_16x16x4_f32 the rank-1 terms (m~_q s_k sum k' and R_q m_k)
+//         already summed over the partitions.  The VALU only converts the integer
+//         products and takes four fused multiply-adds per score (log2 units).
 //   softmax online with a lazily raised reference max; P quantized to 8 bits per
 //         V block (min, scale, round-to-nearest-even codes), staged through LDS.
 //   P'V'  v_mfma_i32_16x16x64_i8: A = P codes, rows = (block, head) block-diagonal
 //         over the span's 4 blocks; B = V codes of 16 channels (lane = channel,
 //         group = block).  One more MFMA with an all-ones B gives the P code sums.
-//         Eq. 4 with the cached V sums: the product term on the VALU, the rank-1
-//         terms through two v_mfma_f32_16x16x4_f32 accumulating into O.
+//         Eq. 4 with the cached V sums: s_p s_v through one fp16 product (s_p in
+//         three pieces), the rank-1 terms through two v_mfma_f32_16x16x4_f32
+//         accumulating into O, the integer product scaled on the VALU.
 //   open block  fp16 values times unquantized probabilities (TAIL_FP16), or its
 //         re-quantized codes with n = T (TAIL_REQUANT).
 // The four waves merge in LDS; when a sequence spans several chunks, each chunk's
@@ -36,6 +39,8 @@ namespace hack {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef float v4f __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 v4h __attribute__((ext_vector_type(4)));
 
 // Operand byte position (4*register + byte) -> element offset within a 16-element
 // slice, for the in-register unpack of 16 codes (b = 2: one dword; b = 4: two).
@@ -104,6 +109,39 @@ __device__ __forceinline__ v4i mfma_i8(v4i a, v4i b, v4i c) {
 __device__ __forceinline__ v4f mfma_f32(float a, float b, v4f c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
+// fp16 matrix-core product with fp32 accumulation, four fp16 values per lane (element 2i
+// in the low half of dword i): k slots 4g .. 4g+3 of lane group g.
+__device__ __forceinline__ v4f mfma_f16k16(u32x2 a, u32x2 b, v4f c) {
+  return __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(v4h, a), __builtin_bit_cast(v4h, b), c, 0, 0, 0);
+}
+
+// x (0 <= |x| < 65504) as three fp16 values h1 + h2 + h3 (h1 = fp16(x), h2 = fp16(x - h1),
+// h3 = fp16(x - h1 - h2); both differences are exact in fp32), packed (h1, h2), (h3, 0).
+// |x - h1 - h2 - h3| <= 2^-33 |x| while all three are normal fp16 values and <= 2^-25
+// otherwise (half the subnormal spacing).  Against an fp16 value y in three k slots of
+// an fp16 product the fp32 accumulator receives x*y to about fp32 accuracy.
+__device__ __forceinline__ u32x2 split3(float x) {
+  const __half h1 = __float2half_rn(x);
+  const float r1 = x - __half2float(h1);
+  const __half h2 = __float2half_rn(r1);
+  const __half h3 = __float2half_rn(r1 - __half2float(h2));
+  return u32x2{(uint32_t)__half_as_ushort(h1) | ((uint32_t)__half_as_ushort(h2) << 16), (uint32_t)__half_as_ushort(h3)};
+}
+// The fp16 value in the high half of w in three k slots: (y, y, y, 0).
+__device__ __forceinline__ u32x2 triple_hi(uint32_t w) {
+  const uint32_t y = w >> 16;
+  return u32x2{y * 0x10001u, y};
+}
+
+// Scores are kept scaled by score_unit<QP>() and the P.V accumulator by kPvUnit: powers
+// of two that lift the small factors s_q (log2 units) and s_p of the fp16 products above
+// fp16's subnormal range without overflowing it: for fp16 inputs s_q <= 2^17 / (2^QP - 1)
+// * 0.128, so score_unit * s_q < 2^14; p~ <= 2^8, so kPvUnit * s_p <= 2^19 / 15 < 2^15.
+template <int QP>
+constexpr float score_unit() {
+  return QP == 8 ? 256.0f : 16.0f;
+}
+constexpr float kPvUnit = 2048.0f, kInvPvUnit = 1.0f / 2048.0f;
 __device__ __forceinline__ float lo_half(uint32_t w) { return __half2float(__ushort_as_half((uint16_t)(w & 0xFFFFu))); }
 __device__ __forceinline__ float hi_half(uint32_t w) { return __half2float(__ushort_as_half((uint16_t)(w >> 16))); }
 
@@ -283,6 +321,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
   constexpr float kInvQmax = 1.0f / kQmax;
   constexpr int kQoff = 1 << (QP - 1);
   constexpr float kQoffF = (float)kQoff;
+  constexpr float kSU = score_unit<QP>(), kInvSU = 1.0f / kSU;  // score unit (see score_unit)
   constexpr int P = D / PI;          // K partitions per token
   constexpr int QPP = 4 / P;         // channel quarters per partition
   constexpr int TILES = PI / 16;     // 16-token tiles per V block
@@ -430,7 +469,8 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
   // m~_q and R of (h, partition of quarter k), divided among the QPP quarters of a
   // partition, so that the rank-1 terms arrive summed over the partitions.
   v4i qa[GT][2];
-  float qs[GT], ra0[GT], ra1[GT];
+  u32x2 qs[GT];
+  float ra0[GT], ra1[GT];
   const int pl = grp / QPP;  // partition of this lane's quarter
   if constexpr (MODE != MODE_PV) {
     const int hh = col >> 2, qq = col & 3;
@@ -442,9 +482,9 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
         qa[rt][m] = qq == grp ? v4i{w.x, w.y, w.z, w.w} : v4i{0, 0, 0, 0};
       }
       constexpr float inv_qpp = 1.0f / (float)QPP;
-      qs[rt] = qq == grp ? qm_lds[rt * 4 + hh][pl][0] : 0.0f;
-      ra0[rt] = qm_lds[rt * 4 + hh][pl][1] * inv_qpp;
-      ra1[rt] = qm_lds[rt * 4 + hh][pl][2] * inv_qpp;
+      qs[rt] = qq == grp ? split3(kSU * qm_lds[rt * 4 + hh][pl][0]) : u32x2{0u, 0u};
+      ra0[rt] = qm_lds[rt * 4 + hh][pl][1] * (inv_qpp * kSU);
+      ra1[rt] = qm_lds[rt * 4 + hh][pl][2] * (inv_qpp * kSU);
     }
   }
 
@@ -592,7 +632,8 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
             v4i acc = v4i{0, 0, 0, 0};
             acc = mfma_i8(qa[rt][0], b0, acc);
             acc = mfma_i8(qa[rt][1], b1, acc);
-            const v4f sqk = mfma_f32(qs[rt], skv, v4f{0.0f, 0.0f, 0.0f, 0.0f});  // s_q s_k per quarter
+            // s_q s_k per quarter (in score units)
+            const v4f sqk = mfma_f16k16(qs[rt], triple_hi(d.km[ti]), v4f{0.0f, 0.0f, 0.0f, 0.0f});
             v4f rk = v4f{0.0f, 0.0f, 0.0f, 0.0f};
             rk = mfma_f32(ra0[rt], bz, rk);   // sum over partitions of m~_q s_k sum k'
             rk = mfma_f32(ra1[rt], mk, rk);   // sum over partitions of R_q m_k
@@ -626,7 +667,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
           float bmax = sv[rt][0];
 #pragma unroll
           for (int tl = 1; tl < TILES; ++tl) bmax = fmaxf(bmax, sv[rt][tl]);
-          bmax = row16_max(bmax);
+          bmax = row16_max(bmax) * kInvSU;  // the scores are in score units
           if (bmax > m_ref[rt] + kMaxSlack || m_ref[rt] == -INFINITY) {  // raise the reference max
             l_run[rt] *= __builtin_amdgcn_exp2f(m_ref[rt] - bmax);
             m_ref[rt] = bmax;
@@ -637,7 +678,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
           float lsum = 0.0f;
 #pragma unroll
           for (int tl = 0; tl < TILES; ++tl) {
-            pt[tl] = __builtin_amdgcn_exp2f(sv[rt][tl] - mr);
+            pt[tl] = __builtin_amdgcn_exp2f(fmaf(sv[rt][tl], kInvSU, -mr));
             lsum += pt[tl];
           }
           l_run[rt] += lsum;
@@ -646,7 +687,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
 #pragma unroll
             for (int tl = 1; tl < TILES; ++tl)
               bmin = fminf(bmin, (full || bt0 + 16 * tl + col < L) ? sv[rt][tl] : INFINITY);
-            bmin = row16_min(bmin);
+            bmin = row16_min(bmin) * kInvSU;
             const float pmax = __builtin_amdgcn_exp2f(bmax - mr);
             const float pmin = __builtin_amdgcn_exp2f(bmin - mr);
             const float dp = pmax - pmin;
@@ -689,7 +730,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
             const float f = __builtin_amdgcn_exp2f(m_blk[rt][k] - m_ref[rt]);
             wl.pst[rt][k][0][grp] = ps_s[rt][k] * f;
             wl.pst[rt][k][1][grp] = (ps_m[rt][k] + kQoffF * ps_s[rt][k]) * f;
-            if (k == kF) wl.tailf[rt][grp] = f;
+            if (k == kF) wl.tailf[rt][grp] = f * kPvUnit;  // O is accumulated in kPvUnit units
           }
           wl.alpha[rt][grp] = __builtin_amdgcn_exp2f(m_start[rt] - m_ref[rt]);
         }
@@ -707,7 +748,8 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
       const float n_g = (float)(vkb < F ? PI : T);
       const int kk = col >> 2, hh = col & 3;
       v4i pa[GT][TILES];
-      float pr0[GT], pr1[GT], pr2[GT];
+      u32x2 pr0[GT];
+      float pr1[GT], pr2[GT];
 #pragma unroll
       for (int rt = 0; rt < GT; ++rt) {
 #pragma unroll
@@ -735,9 +777,11 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
         const float zp[4] = {(float)sacc[0], (float)sacc[1], (float)sacc[2], (float)sacc[3]};
         // rank-1 coefficients, block-diagonal: lane (row kk*4+hh, group g) non-zero for kk == g
         // (such a lane's own registers hold the sums of block g = kk)
-        pr0[rt] = kk == grp ? wl.pst[rt][kk][0][hh] : 0.0f;                  // s_p
-        pr1[rt] = pr0[rt] * pick4(zp, hh);                                   // s_p * sum p~'
-        pr2[rt] = kk == grp ? wl.pst[rt][kk][1][hh] : 0.0f;                 // m~_p = m_p + qoff s_p
+        // all P-side factors in kPvUnit units (O is accumulated in them)
+        const float sp = kk == grp ? wl.pst[rt][kk][0][hh] * kPvUnit : 0.0f;  // s_p
+        pr0[rt] = split3(sp);                                                  // s_p in three fp16 pieces
+        pr1[rt] = sp * pick4(zp, hh);                                          // s_p * sum p~'
+        pr2[rt] = kk == grp ? wl.pst[rt][kk][1][hh] * kPvUnit : 0.0f;        // m~_p = m_p + qoff s_p
       }
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
@@ -754,7 +798,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
           for (int sl = 0; sl < TILES; ++sl) acc = mfma_i8(pa[rt][sl], unpack16<BITS>(vcr + j * VW + sl * SW), acc);
           // Eq. 4: s_p s_v D~ + (s_p sum p~') m_v + m~_p (s_v sum v' + n m_v); the
           // diagonal s_p against the lane's own s_v gives s_p s_v at (block g, head i)
-          const v4f spv = mfma_f32(pr0[rt], svj, v4f{0.0f, 0.0f, 0.0f, 0.0f});
+          const v4f spv = mfma_f16k16(pr0[rt], triple_hi(vmr[j]), v4f{0.0f, 0.0f, 0.0f, 0.0f});
           o_acc[rt][j] = mfma_f32(pr1[rt], mv, o_acc[rt][j]);
           o_acc[rt][j] = mfma_f32(pr2[rt], vbar, o_acc[rt][j]);
 #pragma unroll
@@ -825,7 +869,8 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
   for (int rt = 0; rt < GT; ++rt) {
     float ov[8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) ov[j] = reduce_scatter4(o_acc[rt][j][0], o_acc[rt][j][1], o_acc[rt][j][2], o_acc[rt][j][3]);
+    for (int j = 0; j < 8; ++j)
+      ov[j] = kInvPvUnit * reduce_scatter4(o_acc[rt][j][0], o_acc[rt][j][1], o_acc[rt][j][2], o_acc[rt][j][3]);
     const float lsum = row16_sum(l_run[rt]);
     // lane group g writes head slot 4*rt + g: channels 8*col .. 8*col+7
     float* dst = &wl.mrg_o[rt * 4 + grp][8 * col];
