@@ -101,7 +101,7 @@ def parse():
     ap.add_argument("--no-prefill", action="store_true")
     ap.add_argument("--prefill-iters", type=int, default=10)
     ap.add_argument("--workload", choices=["decode_tiny_l256", "decode_70b_ragged", "decode_long_l131072",
-                                           "sweep_bits_partition"],
+                                           "sweep_bits_partition", "sweep_prefill_partition"],
                     default=None,
                     help="time another decode workload instead (one JSON line per configuration; "
                          "not the headline line)")
@@ -455,6 +455,15 @@ def main():
     if args.only == "copy":
         copy_calibration()
         return
+    if args.workload == "sweep_prefill_partition":
+        # the causal prefill workload's shapes for each code width and partition
+        for bits in (4, 2):
+            for part in (32, 64, 128):
+                res = bench_prefill(max(3, args.prefill_iters // 2), 8, 0, bits, part)
+                print(json.dumps({"workload": "sweep_prefill_partition", "kv_bits": bits, "partition": part,
+                                  "attend_ms": res.get("attend_ms"), "TOPS": res.get("roofline", {}).get("achieved"),
+                                  "frac_of_5POPS": res.get("roofline", {}).get("frac")}), flush=True)
+        return
     if args.workload is not None:
         bench_workload(args.workload, args.steps, args.warmup)
         return
@@ -514,17 +523,19 @@ def main():
     print(json.dumps(result), flush=True)
 
 
-def bench_prefill(iters: int, qp_bits: int = 8, rounding: int = 0):
+def bench_prefill(iters: int, qp_bits: int = 8, rounding: int = 0, kv_bits: int = 0, partition: int = 0):
     """Causal prefill (batch 1, 32/8 heads, 8192 tokens, 4-bit K/V, partition 64, Q/P
-    codes of qp_bits bits): quantize-on-write of the prompt's K/V then attention; int8
-    ops of the causal triangle = 2 products x 32 heads x L(L+1)/2 x 128 x 2."""
+    codes of qp_bits bits; kv_bits / partition override the code width and partition):
+    quantize-on-write of the prompt's K/V then attention; int8 ops of the causal
+    triangle = 2 products x 32 heads x L(L+1)/2 x 128 x 2."""
     import torch
     from paper_2502_03589_amd import hack as hk
     from paper_2502_03589_amd import synth
     wl = synth.WORKLOADS["prefill_l8192"]
     B, Hq, H, d, L = wl.batch, wl.q_heads, wl.kv_heads, wl.head_dim, wl.context
     dev = torch.device("cuda:0")
-    lay = hk.hack_kv_layout_make(d, H, wl.kv_bits, wl.partition, L, qp_bits, rounding, wl.seed)
+    kvb, part = kv_bits or wl.kv_bits, partition or wl.partition
+    lay = hk.hack_kv_layout_make(d, H, kvb, part, L, qp_bits, rounding, wl.seed)
     c = hk.KVCache(lay, B, B, None, dev)
     k = torch.from_numpy(synth.normal_f16(wl.seed, "k", (B, H, L, d))).to(dev)
     v = torch.from_numpy(synth.normal_f16(wl.seed, "v", (B, H, L, d))).to(dev)
@@ -553,7 +564,7 @@ def bench_prefill(iters: int, qp_bits: int = 8, rounding: int = 0):
     a_ms = float(np.median(at))
     q_ms = float(np.median(qt))
     tops = ops / (a_ms * 1e-3) / 1e12
-    q_gbs = quantize_bytes(B, H, L, d, wl.kv_bits, wl.partition, lay.sum_bytes) / (q_ms * 1e-3) / 1e9
+    q_gbs = quantize_bytes(B, H, L, d, kvb, part, lay.sum_bytes) / (q_ms * 1e-3) / 1e9
     return {"workload": "prefill_l8192", "qp_bits": qp_bits, "rounding": "stochastic" if rounding else "nearest",
             "int8_ops": ops, "attend_ms": round(a_ms, 4),
             "quantize_ms": round(q_ms, 4), "quantize_GBs": round(q_gbs, 1),

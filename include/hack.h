@@ -244,8 +244,9 @@ hack_status hack_decode_step(const hack_kv_layout* layout, const hack_kv_cache* 
  * hack_quantize with all seq_lens = len.  q_dev: fp16 [batch][H_q][len][head_dim];
  * out_dev: fp32 [batch][H_q][len][head_dim].  causal != 0 masks token j > i for
  * query i; the masked zeros of P inside a block are quantized with the block.  The
- * open V block is used in fp16.  Requires head_dim 128, partition 32 or 64
- * (128 is decode only), H_q % H_kv == 0, H_q/H_kv <= 8 and batch <= 65535 (else HACK_ERR_UNSUPPORTED). */
+ * open V block is used in fp16.  Requires head_dim 128, partition 32, 64 or 128, cached
+ * code sums, H_q % H_kv == 0, H_q/H_kv <= 8 and batch <= 65535 (else
+ * HACK_ERR_UNSUPPORTED). */
 hack_status hack_attend_prefill(const hack_kv_layout* layout, const hack_kv_cache* cache,
                                 const void* q_dev, int32_t num_q_heads, int32_t batch, int32_t len,
                                 int32_t causal, float* out_dev, hipStream_t stream);

@@ -360,7 +360,6 @@ hack_status hack_attend_prefill(const hack_kv_layout* layout, const hack_kv_cach
   const hack_status sh = attention_shape(layout, num_q_heads);
   if (sh != HACK_OK) return sh;
   if (layout->sum_bytes == 0) return HACK_ERR_UNSUPPORTED;  // prefill reads cached sums
-  if (layout->partition == 128) return HACK_ERR_UNSUPPORTED;  // decode only
   if (batch > kMaxGridYZ) return HACK_ERR_UNSUPPORTED;  // one grid plane per sequence
   const int64_t cap = cache_capacity(layout, cache, batch);
   if (cap < 0) return HACK_ERR_INVALID_ARGUMENT;
@@ -408,7 +407,7 @@ hack_status hack_prefill_from_embeddings(const hack_kv_layout* layout, const hac
   if (num_q_heads < 1 || num_q_heads % layout->num_kv_heads != 0) return HACK_ERR_INVALID_ARGUMENT;
   const hack_status sh = attention_shape(layout, num_q_heads);
   if (sh != HACK_OK) return sh;
-  if (layout->sum_bytes == 0 || layout->partition == 128 || batch > kMaxGridYZ) return HACK_ERR_UNSUPPORTED;
+  if (layout->sum_bytes == 0 || batch > kMaxGridYZ) return HACK_ERR_UNSUPPORTED;
   hack_status st = hack_project_qkv(layout, cache, e_dev, w_dev, num_q_heads, hidden, batch, len, q_out_dev, stream);
   if (st != HACK_OK) return st;
   return hack_attend_prefill(layout, cache, q_out_dev, num_q_heads, batch, len, causal, out_dev, stream);

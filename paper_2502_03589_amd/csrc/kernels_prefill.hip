@@ -47,9 +47,11 @@ struct PrefillCfg {
   static constexpr int TL = PI / 16;  // 16-token tiles per block
   static constexpr int KSL = PI / 4;  // operand bytes per lane per MFMA (k-slots of a lane group)
   // LDS row strides of the unpacked K and V codes (bytes); the 32-byte pads were the
-  // best of a padding sweep of LDS bank conflicts
-  static constexpr int KROW = D + 32;
-  static constexpr int VROW = PI + 32;
+  // best of a padding sweep of LDS bank conflicts.  At partition 128 a 16-byte pad keeps
+  // two workgroups' double-buffered 128-token stages within a compute unit's LDS.
+  static constexpr int PAD = PI == 128 ? 16 : 32;
+  static constexpr int KROW = D + PAD;
+  static constexpr int VROW = PI + PAD;
 };
 
 // int8 MFMA with K = PI: 16x16x64 (16 bytes per lane) or 16x16x32 (8 bytes per lane).
@@ -68,6 +70,29 @@ struct Op<64> {
   static __device__ __forceinline__ v4i ones() { return v4i{0x01010101, 0x01010101, 0x01010101, 0x01010101}; }
   static __device__ __forceinline__ v4i from(const uint32_t* w) {
     return v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
+  }
+};
+// partition 128: one partition is two 16x16x64 products over the lane's 32 bytes (bytes
+// 0-15 of each operand against each other, then bytes 16-31), i.e. a 16x16x128 product
+template <>
+struct Op<128> {
+  struct T {
+    v4i lo, hi;
+  };
+  static __device__ __forceinline__ v4i mfma(T a, T b, v4i c) {
+    c = __builtin_amdgcn_mfma_i32_16x16x64_i8(a.lo, b.lo, c, 0, 0, 0);
+    return __builtin_amdgcn_mfma_i32_16x16x64_i8(a.hi, b.hi, c, 0, 0, 0);
+  }
+  static __device__ __forceinline__ T lds(const int8_t* p) {
+    const int4 w0 = reinterpret_cast<const int4*>(p)[0], w1 = reinterpret_cast<const int4*>(p)[1];
+    return T{v4i{w0.x, w0.y, w0.z, w0.w}, v4i{w1.x, w1.y, w1.z, w1.w}};
+  }
+  static __device__ __forceinline__ T ones() {
+    const v4i o = v4i{0x01010101, 0x01010101, 0x01010101, 0x01010101};
+    return T{o, o};
+  }
+  static __device__ __forceinline__ T from(const uint32_t* w) {
+    return T{v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]}, v4i{(int)w[4], (int)w[5], (int)w[6], (int)w[7]}};
   }
 };
 template <>
@@ -288,8 +313,16 @@ __device__ __forceinline__ void stage_store(const StageRegs<BITS, PI>& r, Stage<
 // that one workgroup's block barrier and staging overlap the other's arithmetic
 // (measured 1.61 -> 1.36-1.44 ms on the 8K causal prefill).
 // SR: the Q and P codes are rounded stochastically (the layout's rounding mode).
+// Partition 128 (eight 16-token tiles per V block, twice the scores and P codes per lane)
+// needs more than 128 VGPRs: one workgroup per compute unit, two waves per SIMD.
+template <int PI>
+constexpr int prefill_waves_per_simd() {
+  return PI == 128 ? 2 : 4;
+}
+
 template <int BITS, int PI, bool SR>
-__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4))) void prefill_kernel(PrefillArgs a) {
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(prefill_waves_per_simd<PI>(),
+                                                                     prefill_waves_per_simd<PI>()))) void prefill_kernel(PrefillArgs a) {
   using C = PrefillCfg<PI>;
   using OP = Op<PI>;
   typedef typename OP::T opT;
@@ -621,6 +654,8 @@ hipError_t launch_prefill(const hack_kv_layout& lay, const CacheView& c, const _
     case 2064: return prefill_impl<2, 64>(a, batch, sr, stream);
     case 4032: return prefill_impl<4, 32>(a, batch, sr, stream);
     case 4064: return prefill_impl<4, 64>(a, batch, sr, stream);
+    case 2128: return prefill_impl<2, 128>(a, batch, sr, stream);
+    case 4128: return prefill_impl<4, 128>(a, batch, sr, stream);
     default: return hipErrorInvalidValue;
   }
 }

@@ -40,6 +40,11 @@ CASES = [
     (2, 32, 4, 1, 300, False, 64, 8),
     (4, 64, 4, 2, 200, True, 0, 4),
     (2, 32, 8, 1, 131, False, 0, 4),
+    # partition 128: one K partition per token, 128-token V blocks, u16 code sums
+    (2, 128, 4, 2, 300, True, 0, 8),
+    (4, 128, 4, 1, 129, False, 0, 8),
+    (4, 128, 8, 1, 200, True, 256, 8),
+    (2, 128, 2, 2, 127, True, 0, 4),
 ]
 
 
