@@ -6,10 +6,14 @@
 // is issued before any of its arithmetic, from wave-uniform section bases plus
 // fixed per-lane offsets.  Per span a wave computes, for up to 4 query heads of the
 // kv group per row tile:
-//   Q'K'  v_mfma_i32_16x16x64_i8: A = Q codes minus 2^(b-1) (signed) with rows
-//         (head h, channel quarter q), block-diagonal so that lane group g only
-//         carries quarter g; B = 2/4-bit K codes unpacked in registers (lane = token,
+//   Q'K'  rows (head h, channel quarter q), block-diagonal so that each quarter meets
+//         only its own K channels; B = the K codes of the lane's token (lane = token,
 //         group = quarter).  Lane (t, g) receives the four quarter products of head g.
+//         2-bit K: v_mfma_f32_16x16x128_f8f6f4 with the codes as e2m1 values c/2 (one
+//         mask and shift per 8 codes, no conversion of the products) against the Q codes
+//         as two e4m3 pieces 16*(q >> 4) and q & 15 (both exact), fp32 sums that are exact.
+//         4-bit K: v_mfma_i32_16x16x64_i8 with Q codes minus 2^(b-1) (signed) and the
+//         codes unpacked to bytes.
 //   Eq. 4 matrix-core products with B = the lane's own K partition metadata spread
 //         it over the output layout: v_mfma_f32_16x16x16_f16 gives s_q s_k per (head,
 //         quarter) from s_q as three fp16 pieces against the stored fp16 s_k (as
@@ -113,6 +117,33 @@ __device__ __forceinline__ v4f mfma_f32(float a, float b, v4f c) {
 // in the low half of dword i): k slots 4g .. 4g+3 of lane group g.
 __device__ __forceinline__ v4f mfma_f16k16(u32x2 a, u32x2 b, v4f c) {
   return __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(v4h, a), __builtin_bit_cast(v4h, b), c, 0, 0, 0);
+}
+
+typedef int v8i __attribute__((ext_vector_type(8)));
+// 16x16x128 matrix-core product of fp8 (e4m3) A and fp4 (e2m1) B with fp32 accumulation.
+// Lane (row or column l % 16, group g): the fp4 operand holds k = 32g .. 32g+31 in nibble
+// order (its dwords 0-3); the fp8 operand holds k = 16g .. 16g+15 in dwords 0-3 and k =
+// 64+16g .. 64+16g+15 in dwords 4-7.  Zero scale arguments select the unscaled instruction
+// (no block scaling, measured identical to unit E8M0 scales): the scaled form keeps its
+// scales in a VGPR, which the compiler was seen to rematerialize inside divergent code,
+// leaving the lanes masked there with stale scales for the whole-wave product.
+__device__ __forceinline__ v4f mfma_f8f4(v8i a, v8i b, v4f c) {
+  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 4, 0, 0, 0, 0);
+}
+// e4m3 encoding of an integer 0 <= v <= 15 (exact).
+__device__ __forceinline__ uint32_t e4m3_int(uint32_t v) {
+  if (v == 0) return 0u;
+  const uint32_t e = 31u - (uint32_t)__builtin_clz(v);
+  return ((e + 7u) << 3) | ((v << 3 >> e) & 7u);
+}
+// A 2-bit code c placed in a nibble is the e2m1 value c / 2.  One dword of 16 codes ->
+// two operand dwords: nibble i of the first = code 2i, of the second = code 2i + 1.  Within
+// a quarter's 32 k slots, slot f therefore holds channel fp4_channel(f).
+__device__ __forceinline__ constexpr int fp4_channel(int f) {
+  return (f & 16) | ((f & 7) << 1) | ((f >> 3) & 1);
+}
+__device__ __forceinline__ constexpr int fp4_slot(int ch) {  // inverse of fp4_channel
+  return (ch & 16) | ((ch & 1) << 3) | ((ch >> 1) & 7);
 }
 
 // x (0 <= |x| < 65504) as three fp16 values h1 + h2 + h3 (h1 = fp16(x), h2 = fp16(x - h1),
@@ -336,7 +367,11 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
 
   // Q codes - qoff per (head slot, quarter, 16-channel slice), each slice already in
   // the byte order of the K operand's in-register unpack
-  __shared__ __attribute__((aligned(16))) int8_t q_lds[HT][4][2][16];
+  // 2-bit K: Q'K' runs on fp8 x fp4 products (K codes need only a nibble spread, the
+  // products arrive in fp32); Q codes enter as e4m3 pieces 16*(q >> 4) and q & 15
+  constexpr bool F4 = BITS == 2;
+  __shared__ __attribute__((aligned(16))) int8_t q_lds[F4 ? 1 : HT][4][2][16];
+  __shared__ __attribute__((aligned(16))) uint8_t q8_lds[2][F4 ? HT : 1][4][32];
   __shared__ float qm_lds[HT][4][3];
   __shared__ __attribute__((aligned(16))) WaveLds<BITS, PI, GT> wl_all[kWaves];
   __shared__ float mrg_ml[kWaves][HT][2];
@@ -440,14 +475,24 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
       {
         const int ch = 2 * lane;  // channels ch, ch + 1 share quarter and slice
         const int g = ch >> 5, m = (ch >> 4) & 1, e = ch & 15;
-        q_lds[gh][g][m][perm_position<BITS>(e)] = real ? (int8_t)((int)c0 - kQoff) : (int8_t)0;
-        q_lds[gh][g][m][perm_position<BITS>(e + 1)] = real ? (int8_t)((int)c1 - kQoff) : (int8_t)0;
+        if constexpr (F4) {
+          const uint32_t u0 = real ? (uint32_t)c0 : 0u, u1 = real ? (uint32_t)c1 : 0u;
+          const int f0 = fp4_slot(ch & 31), f1 = fp4_slot((ch + 1) & 31);
+          q8_lds[0][gh][g][f0] = (uint8_t)((u0 >> 4) ? e4m3_int(u0 >> 4) + 0x20u : 0u);  // 16 * (q >> 4)
+          q8_lds[0][gh][g][f1] = (uint8_t)((u1 >> 4) ? e4m3_int(u1 >> 4) + 0x20u : 0u);
+          q8_lds[1][gh][g][f0] = (uint8_t)e4m3_int(u0 & 15u);
+          q8_lds[1][gh][g][f1] = (uint8_t)e4m3_int(u1 & 15u);
+        } else {
+          q_lds[gh][g][m][perm_position<BITS>(e)] = real ? (int8_t)((int)c0 - kQoff) : (int8_t)0;
+          q_lds[gh][g][m][perm_position<BITS>(e + 1)] = real ? (int8_t)((int)c1 - kQoff) : (int8_t)0;
+        }
       }
       const int p = (2 * lane) / PI;
       if ((2 * lane) % PI == 0) {
         // per partition: s_q, m~_q = m_q + qoff s_q, R = s_q sum q' + n m_q (all in log2 units)
         qm_lds[gh][p][0] = real ? kScoreScale * sq : 0.0f;
-        qm_lds[gh][p][1] = real ? kScoreScale * (mn + kQoffF * sq) : 0.0f;
+        // the fp8 products take the unsigned codes: m_q in place of m~_q
+        qm_lds[gh][p][1] = real ? kScoreScale * (F4 ? mn : mn + kQoffF * sq) : 0.0f;
         qm_lds[gh][p][2] = real ? kScoreScale * (sq * (float)csum + (float)PI * mn) : 0.0f;
         if (MODE == MODE_QK && real && split == 0) {
           a.dbg_qmeta[(((int64_t)s * Hq + hq) * P + p) * 2 + 0] = mn;
@@ -468,7 +513,12 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
   // diagonal q == k, so s_q s_k lands at (lane group h, register q); ra0 / ra1 =
   // m~_q and R of (h, partition of quarter k), divided among the QPP quarters of a
   // partition, so that the rank-1 terms arrive summed over the partitions.
-  v4i qa[GT][2];
+  // With fp8 x fp4 products (2-bit K) the quarter q of row (h, q) occupies k slots 32q ..
+  // 32q+31, which the fp8 operand spreads over lane groups 2(q mod 2), 2(q mod 2) + 1 in
+  // dwords 0-3 (q < 2) or 4-7 (q >= 2); those products carry K codes as e2m1 values c/2,
+  // so s_q is doubled.
+  v4i qa[F4 ? 1 : GT][2];
+  v8i q8h[F4 ? GT : 1], q8l[F4 ? GT : 1];
   u32x2 qs[GT];
   float ra0[GT], ra1[GT];
   const int pl = grp / QPP;  // partition of this lane's quarter
@@ -476,13 +526,24 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
     const int hh = col >> 2, qq = col & 3;
 #pragma unroll
     for (int rt = 0; rt < GT; ++rt) {
+      if constexpr (F4) {
+        const bool lo_half = qq == (grp >> 1), hi_half = qq == 2 + (grp >> 1);
+        int4 wh = int4{0, 0, 0, 0}, wl = int4{0, 0, 0, 0};
+        if (lo_half || hi_half) {
+          wh = *reinterpret_cast<const int4*>(&q8_lds[0][rt * 4 + hh][qq][16 * (grp & 1)]);
+          wl = *reinterpret_cast<const int4*>(&q8_lds[1][rt * 4 + hh][qq][16 * (grp & 1)]);
+        }
+        q8h[rt] = lo_half ? v8i{wh.x, wh.y, wh.z, wh.w, 0, 0, 0, 0} : v8i{0, 0, 0, 0, wh.x, wh.y, wh.z, wh.w};
+        q8l[rt] = lo_half ? v8i{wl.x, wl.y, wl.z, wl.w, 0, 0, 0, 0} : v8i{0, 0, 0, 0, wl.x, wl.y, wl.z, wl.w};
+      } else {
 #pragma unroll
-      for (int m = 0; m < 2; ++m) {
-        const int4 w = *reinterpret_cast<const int4*>(&q_lds[rt * 4 + hh][grp][m][0]);
-        qa[rt][m] = qq == grp ? v4i{w.x, w.y, w.z, w.w} : v4i{0, 0, 0, 0};
+        for (int m = 0; m < 2; ++m) {
+          const int4 w = *reinterpret_cast<const int4*>(&q_lds[rt * 4 + hh][grp][m][0]);
+          qa[rt][m] = qq == grp ? v4i{w.x, w.y, w.z, w.w} : v4i{0, 0, 0, 0};
+        }
       }
       constexpr float inv_qpp = 1.0f / (float)QPP;
-      qs[rt] = qq == grp ? split3(kSU * qm_lds[rt * 4 + hh][pl][0]) : u32x2{0u, 0u};
+      qs[rt] = qq == grp ? split3((F4 ? 2.0f * kSU : kSU) * qm_lds[rt * 4 + hh][pl][0]) : u32x2{0u, 0u};
       ra0[rt] = qm_lds[rt * 4 + hh][pl][1] * (inv_qpp * kSU);
       ra1[rt] = qm_lds[rt * 4 + hh][pl][2] * (inv_qpp * kSU);
     }
@@ -615,8 +676,16 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
 #pragma unroll
         for (int tl = 0; tl < TILES; ++tl) {
           const int ti = k * TILES + tl;
-          const v4i b0 = unpack16<BITS>(d.kc[ti]);
-          const v4i b1 = unpack16<BITS>(d.kc[ti] + SW);
+          v4i b0, b1;
+          v8i b8;
+          if constexpr (F4) {
+            const uint32_t w0 = d.kc[ti][0], w1 = d.kc[ti][1];
+            b8 = v8i{(int)(w0 & 0x33333333u), (int)((w0 >> 2) & 0x33333333u), (int)(w1 & 0x33333333u),
+                     (int)((w1 >> 2) & 0x33333333u), 0, 0, 0, 0};
+          } else {
+            b0 = unpack16<BITS>(d.kc[ti]);
+            b1 = unpack16<BITS>(d.kc[ti] + SW);
+          }
           // the lane's own K partition: m_k, s_k and the cached code sum
           const float mk = lo_half(d.km[ti]), skv = hi_half(d.km[ti]);
           uint32_t kzv;  // code sum of the lane's K partition
@@ -629,9 +698,17 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
           const float bz = skv * (float)kzv;
 #pragma unroll
           for (int rt = 0; rt < GT; ++rt) {
+            // quarter products: fp32 sum of q' k' / 2 (unsigned codes) or int32 sum of (q' - qoff) k'
+            v4f accf;
             v4i acc = v4i{0, 0, 0, 0};
-            acc = mfma_i8(qa[rt][0], b0, acc);
-            acc = mfma_i8(qa[rt][1], b1, acc);
+            if constexpr (F4) {
+              accf = QP == 8 ? mfma_f8f4(q8h[rt], b8, v4f{0.0f, 0.0f, 0.0f, 0.0f}) : v4f{0.0f, 0.0f, 0.0f, 0.0f};
+              accf = mfma_f8f4(q8l[rt], b8, accf);
+            } else {
+              acc = mfma_i8(qa[rt][0], b0, acc);
+              acc = mfma_i8(qa[rt][1], b1, acc);
+              accf = v4f{(float)acc[0], (float)acc[1], (float)acc[2], (float)acc[3]};
+            }
             // s_q s_k per quarter (in score units)
             const v4f sqk = mfma_f16k16(qs[rt], triple_hi(d.km[ti]), v4f{0.0f, 0.0f, 0.0f, 0.0f});
             v4f rk = v4f{0.0f, 0.0f, 0.0f, 0.0f};
@@ -639,7 +716,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
             rk = mfma_f32(ra1[rt], mk, rk);   // sum over partitions of R_q m_k
             float sc = rk[0];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) sc = fmaf((float)acc[q], sqk[q], sc);
+            for (int q = 0; q < 4; ++q) sc = fmaf(accf[q], sqk[q], sc);
             if constexpr (MODE == MODE_QK) {
               // integer partition products (unsigned codes) for the test export:
               // quarter q's code sum comes from lane (token, q)
@@ -651,9 +728,9 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
               if (tok < L && gh < Gl) {
 #pragma unroll
                 for (int p = 0; p < P; ++p) {
-                  int v = kQoff * zq[p];
+                  int v = F4 ? 0 : kQoff * zq[p];
 #pragma unroll
-                  for (int q = p * QPP; q < (p + 1) * QPP; ++q) v += acc[q];
+                  for (int q = p * QPP; q < (p + 1) * QPP; ++q) v += F4 ? (int)(2.0f * accf[q]) : acc[q];
                   a.dbg_prod[(((int64_t)s * Hq + hkv * G + head0 + gh) * a.max_len + tok) * P + p] = v;
                 }
               }
