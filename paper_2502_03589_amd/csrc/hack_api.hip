@@ -380,7 +380,7 @@ hack_status hack_project_qkv(const hack_kv_layout* layout, const hack_kv_cache* 
   const int64_t cap = cache_capacity(layout, cache, batch);
   if (cap < 0) return HACK_ERR_INVALID_ARGUMENT;
   if (len > cap) return HACK_ERR_CAPACITY;
-  const int64_t tiles = (int64_t)batch * ((len + 127) / 128) * (num_q_heads + 2 * layout->num_kv_heads);
+  const int64_t tiles = (int64_t)batch * ((len + 255) / 256) * ((num_q_heads + 2 * layout->num_kv_heads + 1) / 2);
   if (tiles > INT32_MAX) return HACK_ERR_UNSUPPORTED;  // one workgroup per tile in a 1-D grid
   if (batch == 0 || len == 0) return HACK_OK;
   hack::ProjectArgs a;

@@ -100,8 +100,9 @@ struct ProjectArgs {
   __half* q;          // [batch][H_q][len][128] query heads out
   int batch, len, hidden, q_heads, kv_heads;
   // filled by launch_project
-  int mtiles;         // 128-token tiles per sequence
-  int ntiles;         // head tiles: H_q + 2 H_kv
+  int mtiles;         // 256-token tiles per sequence
+  int nheads;         // output heads: H_q + 2 H_kv
+  int ntiles;         // channel tiles of two heads: ceil(nheads / 2)
   int64_t total;      // batch * mtiles * ntiles
   int stochastic;
   uint64_t key_k, key_v;
