@@ -105,7 +105,8 @@ def parse():
                     default=None,
                     help="time another decode workload instead (one JSON line per configuration; "
                          "not the headline line)")
-    ap.add_argument("--only", choices=["decode", "llama8b", "long", "prefill", "project", "copy", "cpu"], default=None,
+    ap.add_argument("--only", choices=["decode", "llama8b", "long", "tiny", "prefill", "project", "copy", "cpu"],
+                    default=None,
                     help="profiling aid: run one leg alone (decode = the headline 70B-share decode step; "
                          "copy = plain device copy of a known size, the calibration for HBM byte counters)")
     return ap.parse_args()
@@ -478,6 +479,9 @@ def main():
         return
     if args.only == "long":
         print(json.dumps({"decode_long_l131072": bench_long()}), flush=True)
+        return
+    if args.only == "tiny":
+        print(json.dumps({"decode_tiny_l256": bench_tiny(args.steps, args.warmup)}), flush=True)
         return
     import torch
     torch.cuda.set_device(torch.device("cuda:0"))
