@@ -9,11 +9,11 @@
 //   Q'K'  rows (head h, channel quarter q), block-diagonal so that each quarter meets
 //         only its own K channels; B = the K codes of the lane's token (lane = token,
 //         group = quarter).  Lane (t, g) receives the four quarter products of head g.
-//         2-bit K: v_mfma_f32_16x16x128_f8f6f4 with the codes as e2m1 values c/2 (one
-//         mask and shift per 8 codes, no conversion of the products) against the Q codes
-//         as two e4m3 pieces 16*(q >> 4) and q & 15 (both exact), fp32 sums that are exact.
-//         4-bit K: v_mfma_i32_16x16x64_i8 with Q codes minus 2^(b-1) (signed) and the
-//         codes unpacked to bytes.
+//         2-bit K, partition 32: v_mfma_f32_16x16x128_f8f6f4 with the codes as e2m1
+//         values c/2 (one mask and shift per 8 codes, no conversion of the products)
+//         against the Q codes as two e4m3 pieces 16*(q >> 4) and q & 15 (both exact),
+//         fp32 sums that are exact.  Otherwise v_mfma_i32_16x16x64_i8 with Q codes minus
+//         2^(b-1) (signed) and the codes unpacked to bytes.
 //   Eq. 4 matrix-core products with B = the lane's own K partition metadata spread
 //         it over the output layout: v_mfma_f32_16x16x16_f16 gives s_q s_k per (head,
 //         quarter) from s_q as three fp16 pieces against the stored fp16 s_k (as
@@ -367,9 +367,12 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
 
   // Q codes - qoff per (head slot, quarter, 16-channel slice), each slice already in
   // the byte order of the K operand's in-register unpack
-  // 2-bit K: Q'K' runs on fp8 x fp4 products (K codes need only a nibble spread, the
-  // products arrive in fp32); Q codes enter as e4m3 pieces 16*(q >> 4) and q & 15
-  constexpr bool F4 = BITS == 2;
+  // 2-bit K at partition 32: Q'K' runs on fp8 x fp4 products (K codes need only a nibble
+  // spread, the products arrive in fp32); Q codes enter as e4m3 pieces 16*(q >> 4) and
+  // q & 15.  At partition 64 a span holds twice the tiles and the 32-cycle fp8 products
+  // cost more than the unpack they save (measured 22.4 against 19.3 us on the 4K
+  // workload), so the int8 path stays there.
+  constexpr bool F4 = BITS == 2 && PI == 32;
   __shared__ __attribute__((aligned(16))) int8_t q_lds[F4 ? 1 : HT][4][2][16];
   __shared__ __attribute__((aligned(16))) uint8_t q8_lds[2][F4 ? HT : 1][4][32];
   __shared__ float qm_lds[HT][4][3];
