@@ -105,6 +105,26 @@ def test_project_bit_exact_where_the_projection_is_exact(bits, pi, paged, roundi
         assert np.array_equal(raw[name][mask], ref[name][mask]), name
 
 
+@pytest.mark.parametrize("B,Hkv,G,bits,pi,L", [(1, 1, 3, 2, 32, 300), (2, 3, 1, 4, 64, 520)])
+def test_project_odd_head_counts_bit_exact(B, Hkv, G, bits, pi, L):
+    """Output heads are computed two to a tile: 5 and 9 heads give tiles that mix a query
+    and a key head, and a last tile with a single value head (its second half reads
+    clamped weight rows and is never stored)."""
+    gu = _gpu()
+    from paper_2502_03589_amd import hack as hk
+    gu.announce(f"project odd heads B={B} Hkv={Hkv} G={G} bits={bits} pi={pi} L={L}")
+    pc = ProjCase(gu, 90 + Hkv + G, B, Hkv, G, L, 192, bits, pi, exact=True)
+    q = hk.hack_project_qkv(pc.layout, pc.cache, pc.e_dev, pc.w_dev, pc.Hq)
+    Qref, seqs = pc.oracle()
+    case, raw = _cache_view(gu, pc)
+    assert np.array_equal(q.cpu().numpy().view(np.uint16), Qref.view(np.uint16))
+    ref = O.pack_cache(seqs, pc.H, 128, bits, pi, pc.page_tokens, pc.num_pages, pc.table_np, pc.B)
+    km, vm, tm = gu.valid_masks(case, include_open_block=True)
+    for name, mask in (("k_codes", km), ("k_meta", km), ("k_sums", km), ("v_codes", vm), ("v_meta", vm),
+                       ("v_sums", vm), ("v_tail", tm)):
+        assert np.array_equal(raw[name][mask], ref[name][mask]), name
+
+
 def _ulps(a, b):
     """|a - b| in fp16 units in the last place (both finite, compared as ordered ints)."""
     ia = a.view(np.int16).astype(np.int32)
