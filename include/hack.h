@@ -149,7 +149,8 @@ int64_t hack_kv_bytes(const hack_kv_layout* layout, int64_t count, int32_t secti
  * 0 <= seq_lens[s] <= max_len.  Writes, for every sequence, the K codes/meta/sums of
  * tokens [0, len), the V codes/meta/sums of the full blocks, the open block both
  * re-quantized (n = T) at its block slot and in fp16 in V_TAIL.  Nothing outside these
- * slots is written.  HACK_ERR_CAPACITY if max_len exceeds the per-sequence capacity. */
+ * slots is written.  HACK_ERR_CAPACITY if max_len exceeds the per-sequence capacity;
+ * HACK_ERR_UNSUPPORTED if batch * H_kv * ceil(max_len / partition) exceeds 2^31 - 1. */
 hack_status hack_quantize(const hack_kv_layout* layout, const hack_kv_cache* cache,
                           const void* k_dev, const void* v_dev, const int32_t* seq_lens_dev,
                           int32_t batch, int32_t max_len, hipStream_t stream);

@@ -193,6 +193,10 @@ hack_status hack_quantize(const hack_kv_layout* layout, const hack_kv_cache* cac
   if (cap < 0) return HACK_ERR_INVALID_ARGUMENT;
   if (max_len > cap) return HACK_ERR_CAPACITY;
   if (batch == 0 || max_len == 0) return HACK_OK;
+  // V blocks are one workgroup (partitions >= 64) or a fixed group of threads each: the
+  // grid must fit its 2^31 - 1 limit
+  if ((int64_t)batch * layout->num_kv_heads * ((max_len + layout->partition - 1) / layout->partition) > INT32_MAX)
+    return HACK_ERR_UNSUPPORTED;
   (void)hipGetLastError();
   return from_hip(hack::launch_quantize(*layout, make_view(layout, cache), static_cast<const __half*>(k_dev),
                                         static_cast<const __half*>(v_dev), seq_lens_dev, batch, max_len, stream));

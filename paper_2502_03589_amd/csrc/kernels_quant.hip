@@ -384,16 +384,16 @@ static hipError_t quantize_impl(const hack_kv_layout& lay, const CacheView& c, c
                        stream, c, k, lens, batch, max_len, stoch, stream_key(lay.seed, 1));
   const int64_t nv = (int64_t)batch * c.kv_heads * ((max_len + PI - 1) / PI) * (c.head_dim / 2);
   const int64_t nblk = (int64_t)batch * c.kv_heads * ((max_len + PI - 1) / PI);
-  if constexpr (PI >= 64) {
-    if (c.head_dim <= 256 && nblk > 0 && nblk <= 0x7FFFFFFF) {  // one workgroup per V block
+  if constexpr (PI >= 64) {  // one workgroup per V block (head_dim <= 256 threads)
+    if (nblk > 0x7FFFFFFF) return hipErrorInvalidValue;
+    if (nblk > 0)
       hipLaunchKernelGGL((quantize_v_split_kernel<BITS, PI>), dim3((unsigned)nblk), dim3(c.head_dim), 0, stream, c,
                          v, lens, max_len, stoch, stream_key(lay.seed, 2));
-      return hipGetLastError();
-    }
+  } else {
+    if (nv > 0)
+      hipLaunchKernelGGL((quantize_v_kernel<BITS, PI>), dim3((unsigned)((nv + 255) / 256)), dim3(256), 0,
+                         stream, c, v, lens, batch, max_len, stoch, stream_key(lay.seed, 2));
   }
-  if (nv > 0)
-    hipLaunchKernelGGL((quantize_v_kernel<BITS, PI>), dim3((unsigned)((nv + 255) / 256)), dim3(256), 0,
-                       stream, c, v, lens, batch, max_len, stoch, stream_key(lay.seed, 2));
   return hipGetLastError();
 }
 

@@ -154,6 +154,15 @@ def test_argument_errors_before_launch(lib):
     assert lib.hack_attend_prefill(L, C, p, 8, 2, 0, 1, p, None) == 0
 
 
+def test_quantize_grid_limit_checked_before_launch(lib):
+    """At partitions >= 64 every V block is one workgroup: a cache with more than
+    2^31 - 1 blocks is rejected before anything is launched."""
+    lay = hk.hack_kv_layout_make(128, 8, 2, 64, 1 << 16)
+    big = _Fake(pages=1 << 18)
+    p = ctypes.c_void_p(0x5000)
+    assert lib.hack_quantize(ctypes.byref(lay), ctypes.byref(big.struct), p, p, p, 1 << 18, 1 << 16, None) == 2
+
+
 def test_workspace_grows_with_context(lib):
     lay = hk.hack_kv_layout_make(128, 8, 2, 32, 256)
     a = hk.hack_decode_workspace_bytes(lay, 16, 32, 4096)
