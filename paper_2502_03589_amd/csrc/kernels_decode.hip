@@ -26,9 +26,11 @@
 //   P'V'  v_mfma_i32_16x16x64_i8: A = P codes, rows = (block, head) block-diagonal
 //         over the span's 4 blocks; B = V codes of 16 channels (lane = channel,
 //         group = block).  One more MFMA with an all-ones B gives the P code sums.
-//         Eq. 4 with the cached V sums: s_p s_v through one fp16 product (s_p in
-//         three pieces), the rank-1 terms through two v_mfma_f32_16x16x4_f32
-//         accumulating into O, the integer product scaled on the VALU.
+//         Eq. 4 with the cached V sums on the VALU: each output of the P'V' layout
+//         is (block, head) at the lane's channel, and the lane holds that block's V
+//         metadata, so s_p s_v D~ + (s_p sum p~' + n m~_p) m_v + m~_p s_v sum v' is
+//         a multiply and three fused multiply-adds per output (a block-diagonal
+//         matrix-core product would spend four times the slots it uses).
 //   open block  fp16 values times unquantized probabilities (TAIL_FP16), or its
 //         re-quantized codes with n = T (TAIL_REQUANT).
 // The four waves merge in LDS; when a sequence spans several chunks, each chunk's
@@ -164,15 +166,13 @@ __device__ __forceinline__ u32x2 triple_hi(uint32_t w) {
   return u32x2{y * 0x10001u, y};
 }
 
-// Scores are kept scaled by score_unit<QP>() and the P.V accumulator by kPvUnit: powers
-// of two that lift the small factors s_q (log2 units) and s_p of the fp16 products above
-// fp16's subnormal range without overflowing it: for fp16 inputs s_q <= 2^17 / (2^QP - 1)
-// * 0.128, so score_unit * s_q < 2^14; p~ <= 2^8, so kPvUnit * s_p <= 2^19 / 15 < 2^15.
+// Scores are kept scaled by score_unit<QP>(): a power of two that lifts the small factor
+// s_q (log2 units) of the fp16 product above fp16's subnormal range without overflowing
+// it: for fp16 inputs s_q <= 2^17 / (2^QP - 1) * 0.128, so score_unit * s_q < 2^14.
 template <int QP>
 constexpr float score_unit() {
   return QP == 8 ? 256.0f : 16.0f;
 }
-constexpr float kPvUnit = 2048.0f, kInvPvUnit = 1.0f / 2048.0f;
 __device__ __forceinline__ float lo_half(uint32_t w) { return __half2float(__ushort_as_half((uint16_t)(w & 0xFFFFu))); }
 __device__ __forceinline__ float hi_half(uint32_t w) { return __half2float(__ushort_as_half((uint16_t)(w >> 16))); }
 
@@ -185,10 +185,6 @@ __device__ __forceinline__ float reduce_scatter4(float v0, float v1, float v2, f
   const float y = __uint_as_float(b[0]) + __uint_as_float(b[1]);  // groups 0,1: value 1; 2,3: value 3
   const auto c = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(y), false, false);
   return __uint_as_float(c[0]) + __uint_as_float(c[1]);
-}
-
-__device__ __forceinline__ float pick4(const float (&v)[4], int i) {
-  return i == 0 ? v[0] : (i == 1 ? v[1] : (i == 2 ? v[2] : v[3]));
 }
 
 // 1/sqrt(128) * log2(e): scores are kept in log2 units so softmax uses exp2.
@@ -810,7 +806,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
             const float f = __builtin_amdgcn_exp2f(m_blk[rt][k] - m_ref[rt]);
             wl.pst[rt][k][0][grp] = ps_s[rt][k] * f;
             wl.pst[rt][k][1][grp] = (ps_m[rt][k] + kQoffF * ps_s[rt][k]) * f;
-            if (k == kF) wl.tailf[rt][grp] = f * kPvUnit;  // O is accumulated in kPvUnit units
+            if (k == kF) wl.tailf[rt][grp] = f;
           }
           wl.alpha[rt][grp] = __builtin_amdgcn_exp2f(m_start[rt] - m_ref[rt]);
         }
@@ -828,8 +824,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
       const float n_g = (float)(vkb < F ? PI : T);
       const int kk = col >> 2, hh = col & 3;
       v4i pa[GT][TILES];
-      u32x2 pr0[GT];
-      float pr1[GT], pr2[GT];
+      float psp[GT][4], pc1[GT][4], pmt[GT][4];
 #pragma unroll
       for (int rt = 0; rt < GT; ++rt) {
 #pragma unroll
@@ -854,14 +849,17 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
 #pragma unroll
         for (int sl = 0; sl < TILES; ++sl)
           sacc = mfma_i8(pa[rt][sl], v4i{0x01010101, 0x01010101, 0x01010101, 0x01010101}, sacc);
-        const float zp[4] = {(float)sacc[0], (float)sacc[1], (float)sacc[2], (float)sacc[3]};
-        // rank-1 coefficients, block-diagonal: lane (row kk*4+hh, group g) non-zero for kk == g
-        // (such a lane's own registers hold the sums of block g = kk)
-        // all P-side factors in kPvUnit units (O is accumulated in them)
-        const float sp = kk == grp ? wl.pst[rt][kk][0][hh] * kPvUnit : 0.0f;  // s_p
-        pr0[rt] = split3(sp);                                                  // s_p in three fp16 pieces
-        pr1[rt] = sp * pick4(zp, hh);                                          // s_p * sum p~'
-        pr2[rt] = kk == grp ? wl.pst[rt][kk][1][hh] * kPvUnit : 0.0f;        // m~_p = m_p + qoff s_p
+        // The lane's outputs are (block grp, heads 0..3) at its channel: the P-side factors of
+        // its own block.
+        const float4 sp4 = *reinterpret_cast<const float4*>(&wl.pst[rt][grp][0][0]);
+        const float4 mp4 = *reinterpret_cast<const float4*>(&wl.pst[rt][grp][1][0]);
+        const float spa[4] = {sp4.x, sp4.y, sp4.z, sp4.w}, mpa[4] = {mp4.x, mp4.y, mp4.z, mp4.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          psp[rt][i] = spa[i];                                               // s_p
+          pmt[rt][i] = mpa[i];                                               // m~_p = m_p + qoff s_p
+          pc1[rt][i] = fmaf(n_g, pmt[rt][i], psp[rt][i] * (float)sacc[i]);  // s_p sum p~' + n m~_p
+        }
       }
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
@@ -870,19 +868,19 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
         if constexpr (!SE) zj = code_sum<BITS, VW>(vcr + j * VW);
         else if constexpr (SB == 1) zj = (vzr[j >> 2] >> (8 * (j & 3))) & 0xFFu;
         else zj = (vzr[j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
-        const float vbar = fmaf(n_g, mv, svj * (float)zj);  // s_v sum v' + n m_v
+        const float svz = svj * (float)zj;  // s_v sum v'
 #pragma unroll
         for (int rt = 0; rt < GT; ++rt) {
           v4i acc = v4i{0, 0, 0, 0};
 #pragma unroll
           for (int sl = 0; sl < TILES; ++sl) acc = mfma_i8(pa[rt][sl], unpack16<BITS>(vcr + j * VW + sl * SW), acc);
-          // Eq. 4: s_p s_v D~ + (s_p sum p~') m_v + m~_p (s_v sum v' + n m_v); the
-          // diagonal s_p against the lane's own s_v gives s_p s_v at (block g, head i)
-          const v4f spv = mfma_f16k16(pr0[rt], triple_hi(vmr[j]), v4f{0.0f, 0.0f, 0.0f, 0.0f});
-          o_acc[rt][j] = mfma_f32(pr1[rt], mv, o_acc[rt][j]);
-          o_acc[rt][j] = mfma_f32(pr2[rt], vbar, o_acc[rt][j]);
+          // Eq. 4: s_p s_v D~ + (s_p sum p~' + n m~_p) m_v + m~_p s_v sum v'
 #pragma unroll
-          for (int i = 0; i < 4; ++i) o_acc[rt][j][i] = fmaf(spv[i], (float)acc[i], o_acc[rt][j][i]);
+          for (int i = 0; i < 4; ++i) {
+            float o = fmaf(psp[rt][i] * svj, (float)acc[i], o_acc[rt][j][i]);
+            o = fmaf(pc1[rt][i], mv, o);
+            o_acc[rt][j][i] = fmaf(pmt[rt][i], svz, o);
+          }
           if constexpr (MODE == MODE_PV) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
@@ -950,7 +948,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
     float ov[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j)
-      ov[j] = kInvPvUnit * reduce_scatter4(o_acc[rt][j][0], o_acc[rt][j][1], o_acc[rt][j][2], o_acc[rt][j][3]);
+      ov[j] = reduce_scatter4(o_acc[rt][j][0], o_acc[rt][j][1], o_acc[rt][j][2], o_acc[rt][j][3]);
     const float lsum = row16_sum(l_run[rt]);
     // lane group g writes head slot 4*rt + g: channels 8*col .. 8*col+7
     float* dst = &wl.mrg_o[rt * 4 + grp][8 * col];
