@@ -17,10 +17,13 @@
 //   Eq. 4 matrix-core products with B = the lane's own K partition metadata spread
 //         it over the output layout: v_mfma_f32_16x16x16_f16 gives s_q s_k per (head,
 //         quarter) from s_q as three fp16 pieces against the stored fp16 s_k (as
-//         exact as fp32, half the issue cycles of the fp32 product), two
-//         v_mfma_f32_16x16x4_f32 the rank-1 terms (m~_q s_k sum k' and R_q m_k)
-//         already summed over the partitions.  The VALU only converts the integer
-//         products and takes four fused multiply-adds per score (log2 units).
+//         exact as fp32, half the issue cycles of the fp32 product); the rank-1
+//         terms (m~_q s_k sum k' and R_q m_k) arrive already summed over the
+//         partitions, at 2 bits from one v_mfma_f32_16x16x32_f16 (the query-side
+//         factors in fp16 pieces under a power-of-two scale per head, s_k sum k'
+//         split exactly into two fp16 values, m_k as stored), at 4 bits from two
+//         v_mfma_f32_16x16x4_f32.  The VALU converts the integer products and takes
+//         four fused multiply-adds per score (log2 units).
 //   softmax online with a lazily raised reference max; P quantized to 8 bits per
 //         V block (min, scale, round-to-nearest-even codes), staged through LDS.
 //   P'V'  v_mfma_i32_16x16x64_i8: A = P codes, rows = (block, head) block-diagonal
@@ -164,6 +167,29 @@ __device__ __forceinline__ u32x2 split3(float x) {
 __device__ __forceinline__ u32x2 triple_hi(uint32_t w) {
   const uint32_t y = w >> 16;
   return u32x2{y * 0x10001u, y};
+}
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 v8h __attribute__((ext_vector_type(8)));
+// fp16 matrix-core product with fp32 accumulation, eight fp16 values per lane (element
+// 2i in the low half of dword i); A and B pair their elements slot by slot.
+__device__ __forceinline__ v4f mfma_f16k32(u32x4 a, u32x4 b, v4f c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(v8h, a), __builtin_bit_cast(v8h, b), c, 0, 0, 0);
+}
+// x as two fp16 values (hi, lo) packed: hi = x rounded toward zero, lo = x - hi (exact in
+// fp32) rounded toward zero.  For x with at most 21 significant bits (an fp16 value times
+// an integer below 2^10, times a power of two) and lo in fp16's normal range, hi + lo = x.
+__device__ __forceinline__ uint32_t split2_rtz(float x) {
+  const auto t = __builtin_amdgcn_cvt_pkrtz(x, 0.0f);
+  const auto u = __builtin_amdgcn_cvt_pkrtz(x, x - (float)t[0]);
+  return __builtin_bit_cast(uint32_t, u);
+}
+// x as two fp16 values rounded to nearest, (h1, h2) packed: |x - h1 - h2| <= 2^-22 |x|
+// while both are normal.
+__device__ __forceinline__ uint32_t split2(float x) {
+  const __half h1 = __float2half_rn(x);
+  const __half h2 = __float2half_rn(x - __half2float(h1));
+  return (uint32_t)__half_as_ushort(h1) | ((uint32_t)__half_as_ushort(h2) << 16);
 }
 
 // Scores are kept scaled by score_unit<QP>(): a power of two that lifts the small factor
@@ -349,6 +375,13 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
   constexpr int kQoff = 1 << (QP - 1);
   constexpr float kQoffF = (float)kQoff;
   constexpr float kSU = score_unit<QP>(), kInvSU = 1.0f / kSU;  // score unit (see score_unit)
+  // Q'K' rank-1 terms on one fp16 16x16x32 product (2-bit K) or two fp32 16x16x4 products
+  // (4-bit K, whose kernels sit at the register budget of three waves per SIMD: the fp16
+  // operands take three more registers).  2^kRankB (2^BITS - 1) PI <= 1 keeps
+  // s_k sum k' 2^kRankB below fp16's largest value.
+  constexpr bool kRankF16 = BITS == 2;
+  constexpr int kRankB = BITS == 2 ? (PI == 32 ? -7 : -8) : (PI == 32 ? -9 : -10);
+  constexpr float kRankScale = BITS == 2 ? (PI == 32 ? 0x1p-7f : 0x1p-8f) : (PI == 32 ? 0x1p-9f : 0x1p-10f);
   constexpr int P = D / PI;          // K partitions per token
   constexpr int QPP = 4 / P;         // channel quarters per partition
   constexpr int TILES = PI / 16;     // 16-token tiles per V block
@@ -372,6 +405,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
   __shared__ __attribute__((aligned(16))) int8_t q_lds[F4 ? 1 : HT][4][2][16];
   __shared__ __attribute__((aligned(16))) uint8_t q8_lds[2][F4 ? HT : 1][4][32];
   __shared__ float qm_lds[HT][4][3];
+  __shared__ float qu_lds[HT];  // unscale of a head's fp16 rank-1 product
   __shared__ __attribute__((aligned(16))) WaveLds<BITS, PI, GT> wl_all[kWaves];
   __shared__ float mrg_ml[kWaves][HT][2];
 
@@ -487,12 +521,29 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
         }
       }
       const int p = (2 * lane) / PI;
+      // Rank-1 factors of the partition in score units, divided among its QPP quarters:
+      // m~_q = m_q + qoff s_q (the fp8 products take the unsigned codes: m_q) and
+      // R = s_q sum q' + n m_q.  For the fp16 product both are scaled by a power of two
+      // 2^e per head (R by 2^(e + kRankB) more) that brings the head's largest magnitude
+      // into [2^13, 2^14): fp16's range then holds them for any fp16 input.
+      constexpr float kRankUnit = kSU / (float)QPP;
+      float r1 = real ? kScoreScale * (F4 ? mn : mn + kQoffF * sq) * kRankUnit : 0.0f;
+      float r2 = real ? kScoreScale * (sq * (float)csum + (float)PI * mn) * kRankUnit : 0.0f;
+      int qe = 0;
+      if constexpr (kRankF16) {
+        float mx = fmaxf(fabsf(r1), fabsf(r2) * kRankScale);
+#pragma unroll
+        for (int m = PI / 2; m < 64; m <<= 1) mx = fmaxf(mx, __shfl_xor(mx, m, 64));
+        qe = mx > 0.0f ? 14 - __builtin_amdgcn_frexp_expf(mx) : 0;
+        r1 = ldexpf(r1, qe);
+        r2 = ldexpf(r2, qe + kRankB);
+      }
       if ((2 * lane) % PI == 0) {
-        // per partition: s_q, m~_q = m_q + qoff s_q, R = s_q sum q' + n m_q (all in log2 units)
+        // per partition (log2 units): s_q and the rank-1 factors above
         qm_lds[gh][p][0] = real ? kScoreScale * sq : 0.0f;
-        // the fp8 products take the unsigned codes: m_q in place of m~_q
-        qm_lds[gh][p][1] = real ? kScoreScale * (F4 ? mn : mn + kQoffF * sq) : 0.0f;
-        qm_lds[gh][p][2] = real ? kScoreScale * (sq * (float)csum + (float)PI * mn) : 0.0f;
+        qm_lds[gh][p][1] = r1;
+        qm_lds[gh][p][2] = r2;
+        if (kRankF16 && p == 0) qu_lds[gh] = ldexpf(1.0f, -(qe + kRankB));
         if (MODE == MODE_QK && real && split == 0) {
           a.dbg_qmeta[(((int64_t)s * Hq + hq) * P + p) * 2 + 0] = mn;
           a.dbg_qmeta[(((int64_t)s * Hq + hq) * P + p) * 2 + 1] = sq;
@@ -507,11 +558,11 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
   __syncthreads();
 
   // Q operands.  Rows of the QK tile are (head h, quarter q) = 4h + q; the i8
-  // operand of lane (row, group g) is non-zero only for q == g.  The f32 operands
+  // operand of lane (row, group g) is non-zero only for q == g.  The Eq. 4 operands
   // take the lane's group as the summed index k: qs = s_q of (h, quarter k) on the
-  // diagonal q == k, so s_q s_k lands at (lane group h, register q); ra0 / ra1 =
-  // m~_q and R of (h, partition of quarter k), divided among the QPP quarters of a
-  // partition, so that the rank-1 terms arrive summed over the partitions.
+  // diagonal q == k, so s_q s_k lands at (lane group h, register q); the rank-1
+  // operands hold m~_q and R of (h, partition of quarter k), divided among the QPP
+  // quarters of a partition, so that the rank-1 terms arrive summed over the partitions.
   // With fp8 x fp4 products (2-bit K) the quarter q of row (h, q) occupies k slots 32q ..
   // 32q+31, which the fp8 operand spreads over lane groups 2(q mod 2), 2(q mod 2) + 1 in
   // dwords 0-3 (q < 2) or 4-7 (q >= 2); those products carry K codes as e2m1 values c/2,
@@ -519,7 +570,9 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
   v4i qa[F4 ? 1 : GT][2];
   v8i q8h[F4 ? GT : 1], q8l[F4 ? GT : 1];
   u32x2 qs[GT];
-  float ra0[GT], ra1[GT];
+  float ra0[kRankF16 ? 1 : GT], ra1[kRankF16 ? 1 : GT];  // rank-1 A operands (fp32 products)
+  u32x4 ra[kRankF16 ? GT : 1];                            // rank-1 A operand (fp16 product)
+  float run[kRankF16 ? GT : 1];                           // its unscale for head grp
   const int pl = grp / QPP;  // partition of this lane's quarter
   if constexpr (MODE != MODE_PV) {
     const int hh = col >> 2, qq = col & 3;
@@ -541,10 +594,19 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
           qa[rt][m] = qq == grp ? v4i{w.x, w.y, w.z, w.w} : v4i{0, 0, 0, 0};
         }
       }
-      constexpr float inv_qpp = 1.0f / (float)QPP;
       qs[rt] = qq == grp ? split3((F4 ? 2.0f * kSU : kSU) * qm_lds[rt * 4 + hh][pl][0]) : u32x2{0u, 0u};
-      ra0[rt] = qm_lds[rt * 4 + hh][pl][1] * (inv_qpp * kSU);
-      ra1[rt] = qm_lds[rt * 4 + hh][pl][2] * (inv_qpp * kSU);
+      if constexpr (kRankF16) {
+        // per lane group, A slots (m~ hi, m~ hi, m~ lo, m~ lo, R h1, R h2, R h3, 0) of (head,
+        // partition of the quarter) against B slots (b hi, b lo, b hi, b lo, m_k, m_k, m_k,
+        // 0) of (token, partition), b = s_k sum k' 2^kRankB split exactly
+        const uint32_t a0 = split2(qm_lds[rt * 4 + hh][pl][1]);
+        const u32x2 a1 = split3(qm_lds[rt * 4 + hh][pl][2]);
+        ra[rt] = u32x4{(a0 & 0xFFFFu) * 0x10001u, (a0 >> 16) * 0x10001u, a1[0], a1[1]};
+        run[rt] = qu_lds[rt * 4 + grp];
+      } else {
+        ra0[rt] = qm_lds[rt * 4 + hh][pl][1];
+        ra1[rt] = qm_lds[rt * 4 + hh][pl][2];
+      }
     }
   }
 
@@ -686,7 +748,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
             b1 = unpack16<BITS>(d.kc[ti] + SW);
           }
           // the lane's own K partition: m_k, s_k and the cached code sum
-          const float mk = lo_half(d.km[ti]), skv = hi_half(d.km[ti]);
+          const float skv = hi_half(d.km[ti]);
           uint32_t kzv;  // code sum of the lane's K partition
           if constexpr (SE) {
             kzv = d.kz[ti];
@@ -694,7 +756,16 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
             kzv = code_sum<BITS, KW>(d.kc[ti]);
             if constexpr (QPP == 2) kzv += (uint32_t)__shfl_xor((int)kzv, 16, 64);  // the partition's other quarter
           }
-          const float bz = skv * (float)kzv;
+          [[maybe_unused]] float bz, mk;   // s_k sum k' and m_k for the fp32 products
+          [[maybe_unused]] u32x4 rb;       // B operand of the fp16 product
+          if constexpr (kRankF16) {
+            const uint32_t b2 = split2_rtz(skv * ((float)kzv * kRankScale));  // s_k sum k' 2^kRankB
+            const uint32_t mkw = d.km[ti] & 0xFFFFu;                          // m_k (fp16)
+            rb = u32x4{b2, b2, mkw * 0x10001u, mkw};
+          } else {
+            bz = skv * (float)kzv;
+            mk = lo_half(d.km[ti]);
+          }
 #pragma unroll
           for (int rt = 0; rt < GT; ++rt) {
             // quarter products: fp32 sum of q' k' / 2 (unsigned codes) or int32 sum of (q' - qoff) k'
@@ -710,10 +781,14 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
             }
             // s_q s_k per quarter (in score units)
             const v4f sqk = mfma_f16k16(qs[rt], triple_hi(d.km[ti]), v4f{0.0f, 0.0f, 0.0f, 0.0f});
-            v4f rk = v4f{0.0f, 0.0f, 0.0f, 0.0f};
-            rk = mfma_f32(ra0[rt], bz, rk);   // sum over partitions of m~_q s_k sum k'
-            rk = mfma_f32(ra1[rt], mk, rk);   // sum over partitions of R_q m_k
-            float sc = rk[0];
+            // sum over partitions of m~_q s_k sum k' + R_q m_k
+            float sc;
+            if constexpr (kRankF16) {
+              sc = mfma_f16k32(ra[rt], rb, v4f{0.0f, 0.0f, 0.0f, 0.0f})[0] * run[rt];
+            } else {
+              v4f rk = mfma_f32(ra0[rt], bz, v4f{0.0f, 0.0f, 0.0f, 0.0f});
+              sc = mfma_f32(ra1[rt], mk, rk)[0];
+            }
 #pragma unroll
             for (int q = 0; q < 4; ++q) sc = fmaf(accf[q], sqk[q], sc);
             if constexpr (MODE == MODE_QK) {
