@@ -110,6 +110,42 @@ def test_attend_decode_matches_oracle(bits, pi, group, H, lens, tail_mode, paged
             assert np.all(got[b] == 0)
 
 
+@pytest.mark.parametrize("bits,pi", [(2, 32), (2, 64), (4, 32)])
+def test_attend_decode_query_and_key_ranges(bits, pi):
+    """Eq. 4's rank-1 terms over wide ranges: query heads scaled by 1/64 and by 256, one
+    offset by +40 (m~_q and R far from s_q), one with a constant partition (s_q = 0),
+    one nearly constant; keys whose first partition spans 2e-3 (tiny s_k) every third
+    token and whose second is scaled by 30 every fifth.  The fp16 rank-1 product's
+    per-head power-of-two scales and exact splits of s_k sum k' are exercised at both
+    ends of their range."""
+    gu = _gpu()
+    from paper_2502_03589_amd import hack as hk
+    lens = [300, 77]
+    gu.announce(f"decode ranges bits={bits} pi={pi} G=8 lens={lens}")
+    case = gu.Case(4242 + bits + pi, len(lens), 1, lens, bits, pi, group=8)
+    q = case.q.astype(np.float32)
+    q[:, 0] *= 1.0 / 64.0
+    q[:, 1] *= 256.0
+    q[:, 2] += 40.0
+    q[:, 3, :pi] = 0.75
+    q[:, 4] = 0.01 * q[:, 4] + 3.0
+    case.q = q.astype(np.float16)
+    k = case.k.astype(np.float32)
+    k[:, :, ::3, :pi] = 0.5 + 1e-3 * k[:, :, ::3, :pi]
+    k[:, :, 1::5, pi:2 * pi] *= 30.0
+    case.k = k.astype(np.float16)
+    case.quantize()
+    out = hk.hack_attend_decode(case.layout, case.cache, torch.from_numpy(case.q).to(gu.DEV), case.lens_dev,
+                                case.max_len)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    ref = O.attend_decode(case.q, case.oracle_seqs(), 1)
+    assert np.all(np.isfinite(got))
+    err = gu.rel_err(got, ref)
+    print(f"max|d|/|O|inf = {err:.3e}")
+    assert err <= TOL
+
+
 def test_attend_decode_deterministic_and_workspace_reusable():
     gu = _gpu()
     from paper_2502_03589_amd import hack as hk
