@@ -176,13 +176,15 @@ typedef _Float16 v8h __attribute__((ext_vector_type(8)));
 __device__ __forceinline__ v4f mfma_f16k32(u32x4 a, u32x4 b, v4f c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(v8h, a), __builtin_bit_cast(v8h, b), c, 0, 0, 0);
 }
-// x as two fp16 values (hi, lo) packed: hi = x rounded toward zero, lo = x - hi (exact in
-// fp32) rounded toward zero.  For x with at most 21 significant bits (an fp16 value times
-// an integer below 2^10, times a power of two) and lo in fp16's normal range, hi + lo = x.
-__device__ __forceinline__ uint32_t split2_rtz(float x) {
-  const auto t = __builtin_amdgcn_cvt_pkrtz(x, 0.0f);
-  const auto u = __builtin_amdgcn_cvt_pkrtz(x, x - (float)t[0]);
-  return __builtin_bit_cast(uint32_t, u);
+// x as two fp16 values, each in both halves of a dword: (hi, hi) and (lo, lo), hi = x
+// rounded toward zero, lo = x - hi (exact in fp32) rounded toward zero.  For x with at
+// most 21 significant bits (an fp16 value times an integer below 2^10, times a power of
+// two) and lo in fp16's normal range, hi + lo = x.
+__device__ __forceinline__ u32x2 split2_rtz_pairs(float x) {
+  const auto h = __builtin_amdgcn_cvt_pkrtz(x, x);
+  const float r = x - (float)h[0];
+  const auto l = __builtin_amdgcn_cvt_pkrtz(r, r);
+  return u32x2{__builtin_bit_cast(uint32_t, h), __builtin_bit_cast(uint32_t, l)};
 }
 // x as two fp16 values rounded to nearest, (h1, h2) packed: |x - h1 - h2| <= 2^-22 |x|
 // while both are normal.
@@ -596,12 +598,13 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
       }
       qs[rt] = qq == grp ? split3((F4 ? 2.0f * kSU : kSU) * qm_lds[rt * 4 + hh][pl][0]) : u32x2{0u, 0u};
       if constexpr (kRankF16) {
-        // per lane group, A slots (m~ hi, m~ hi, m~ lo, m~ lo, R h1, R h2, R h3, 0) of (head,
-        // partition of the quarter) against B slots (b hi, b lo, b hi, b lo, m_k, m_k, m_k,
-        // 0) of (token, partition), b = s_k sum k' 2^kRankB split exactly
+        // per lane group, A slots (m~ hi, m~ lo, m~ hi, m~ lo, R h1, R h2, R h3, 0) of (head,
+        // partition of the quarter) against B slots (b hi, b hi, b lo, b lo, m_k, m_k, m_k,
+        // s_k) of (token, partition), b = s_k sum k' 2^kRankB split exactly; the last B
+        // dword is the stored (m_k, s_k) word itself
         const uint32_t a0 = split2(qm_lds[rt * 4 + hh][pl][1]);
         const u32x2 a1 = split3(qm_lds[rt * 4 + hh][pl][2]);
-        ra[rt] = u32x4{(a0 & 0xFFFFu) * 0x10001u, (a0 >> 16) * 0x10001u, a1[0], a1[1]};
+        ra[rt] = u32x4{a0, a0, a1[0], a1[1]};
         run[rt] = qu_lds[rt * 4 + grp];
       } else {
         ra0[rt] = qm_lds[rt * 4 + hh][pl][1];
@@ -748,7 +751,6 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
             b1 = unpack16<BITS>(d.kc[ti] + SW);
           }
           // the lane's own K partition: m_k, s_k and the cached code sum
-          const float skv = hi_half(d.km[ti]);
           uint32_t kzv;  // code sum of the lane's K partition
           if constexpr (SE) {
             kzv = d.kz[ti];
@@ -759,11 +761,11 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
           [[maybe_unused]] float bz, mk;   // s_k sum k' and m_k for the fp32 products
           [[maybe_unused]] u32x4 rb;       // B operand of the fp16 product
           if constexpr (kRankF16) {
-            const uint32_t b2 = split2_rtz(skv * ((float)kzv * kRankScale));  // s_k sum k' 2^kRankB
-            const uint32_t mkw = d.km[ti] & 0xFFFFu;                          // m_k (fp16)
-            rb = u32x4{b2, b2, mkw * 0x10001u, mkw};
+            // s_k sum k' 2^kRankB, exact in fp32 (the fp16 s_k enters the FMA unconverted)
+            const u32x2 b = split2_rtz_pairs(fmaf(hi_half(d.km[ti]), (float)kzv * kRankScale, 0.0f));
+            rb = u32x4{b[0], b[1], __builtin_amdgcn_perm(d.km[ti], d.km[ti], 0x01000100u), d.km[ti]};
           } else {
-            bz = skv * (float)kzv;
+            bz = hi_half(d.km[ti]) * (float)kzv;
             mk = lo_half(d.km[ti]);
           }
 #pragma unroll
