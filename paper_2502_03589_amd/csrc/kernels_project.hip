@@ -5,24 +5,26 @@
 // output channels n are the H_q query heads' 128 channels, then the H_kv key heads',
 // then the H_kv value heads'.  One workgroup of eight 64-lane waves computes a tile of
 // 256 tokens x 256 channels, i.e. two heads of 256 tokens of one sequence:
-//   main loop  K steps of 64 input channels; both 256 x 64 fp16 tiles (E rows and W
-//              rows) are staged in LDS (two buffers: the next step's global loads are
-//              in flight while this step's MFMAs run); wave (wm, wn) computes rows
-//              128 wm .. +128 and channels 64 wn .. +64 with v_mfma_f32_32x32x16_f16
-//              (4 x 2 tiles of 32 x 32, fp32 accumulators), so each 16-byte LDS read
-//              feeds 21 multiply-adds per lane (the 64 x 64 wave tile of a 128 x 128
-//              workgroup tile fed 16, the rate at which one compute unit's LDS and its
-//              matrix cores are equally busy), and each fetched byte of E and W serves
-//              twice as many products.
-//   epilogue   the tile is rounded to fp16 into LDS; then, for each of its two heads:
-//              a query head is written out in fp16 (the prefill attention quantizes
-//              Q itself); a key head is quantized per (token, partition) and a value
-//              head per (V block, channel) straight into the cache, with the same
-//              quantizer and element indices as hack_quantize, including the fp16
-//              open V block.  The fp16 K and V never reach device memory.
+//   main loop  K steps of 32 input channels through four LDS stages of 32 KB (the 256 E
+//              rows and the 256 W rows of the step, 64 bytes each, 16-byte chunks
+//              XOR-swizzled so that fragment reads hit distinct banks).  The stages are
+//              filled by direct global-to-LDS loads (global_load_lds_dwordx4, 1 KB per
+//              wave instruction, no registers) issued three steps ahead, so about three
+//              steps of matrix work cover each load's latency; one barrier per step
+//              publishes a stage and frees the one computed before it.  Wave (wm, wn)
+//              computes rows 128 wm .. +128 and channels 64 wn .. +64 with
+//              v_mfma_f32_32x32x16_f16 (4 x 2 tiles of 32 x 32, fp32 accumulators), so
+//              each 16-byte LDS read feeds 21 multiply-adds per lane, and each fetched
+//              byte of E and W serves twice as many products as with 128 x 128 tiles.
+//   epilogue   the tile is rounded to fp16 into the stage buffers; then, for each of its
+//              two heads: a query head is written out in fp16 (the prefill attention
+//              quantizes Q itself); a key head is quantized per (token, partition) and a
+//              value head per (V block, channel) straight into the cache, with the same
+//              quantizer and element indices as hack_quantize, including the fp16 open
+//              V block.  The fp16 K and V never reach device memory.
 // Tiles are numbered so that the workgroups one XCD runs at a time share their E and
 // W tiles (groups of four token tiles per channel tile, contiguous ranges per XCD), so
-// each 64-channel slab is fetched into that XCD's L2 once for several workgroups.
+// each slab is fetched into that XCD's L2 once for several workgroups.
 #include "hack_internal.hpp"
 
 namespace hack {
@@ -31,27 +33,36 @@ namespace {
 
 typedef _Float16 v8h __attribute__((ext_vector_type(8)));
 typedef float v16f __attribute__((ext_vector_type(16)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kBM = 256;          // tokens per tile
 constexpr int kBN = 256;          // output channels per tile (two heads)
-constexpr int kBK = 64;           // input channels per step
+constexpr int kBK = 32;           // input channels per step
 constexpr int kThreads = 512;     // eight waves: 2 (tokens) x 4 (channels)
-constexpr int kRowH = kBK + 8;    // LDS row stride of a staged tile (halves): 144 bytes, so that the
-                                  // eight lanes of an LDS cycle read distinct banks
-constexpr int kTileH = kBN + 8;   // LDS row stride of the fp16 output tile (halves)
+constexpr int kStages = 4;        // LDS stages: loads run three steps ahead of the products
+constexpr int kStageH = (kBM + kBN) * kBK;  // halves per stage: 256 E rows, then 256 W rows, of 64 bytes
+constexpr int kDma = kStageH * 2 / 1024 / (kThreads / 64);  // 1-KB direct-to-LDS loads per wave and step
 constexpr int kGroupM = 4;        // token tiles that share each channel tile in the numbering
 constexpr int kXcds = 8;          // workgroups are dealt to the XCDs round-robin
-constexpr int kPieces = kBM * kBK / 8 / kThreads;  // 16-byte pieces per thread and operand per step
+static_assert(2 * kDma < 16, "the stage waits encode vmcnt in four bits");
+typedef __attribute__((address_space(3))) void lvoid;
 
-struct Stages {
-  __half a[2][kBM][kRowH];
-  __half b[2][kBN][kRowH];
-};
-union ProjectLds {
-  Stages st;
-  __half tile[kBM][kTileH];
-};
+// Position of 16-byte chunk c (0..3) of staged row r: rows are 64 bytes, and chunk c
+// sits at c ^ ((r / 2) mod 4), so the eight rows one LDS cycle reads (32-row fragment
+// reads, eight lanes per cycle) cover all eight 16-byte slots of 128 bytes.
+__device__ __forceinline__ int stage_chunk(int r, int c) { return c ^ ((r >> 1) & 3); }
+
+// 16 bytes per lane from global memory straight into LDS: lane l writes LDS bytes
+// lds + 16 l (lds wave-uniform, via M0).  Issued as inline assembly so that the
+// compiler does not add waits for it before LDS reads of other stages; the kernel
+// waits for each stage's loads explicitly (vmcnt) before the barrier that publishes it.
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
+}
+
+// Workgroup barrier that orders LDS accesses without waiting for outstanding
+// direct-to-LDS loads (a fence would wait for all of them); each wave waits for its
+// own loads of a stage explicitly before it.
+__device__ __forceinline__ void stage_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
 __device__ __forceinline__ v16f mfma_f16(v8h a, v8h b, v16f c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
@@ -61,7 +72,11 @@ __device__ __forceinline__ v16f mfma_f16(v8h a, v8h b, v16f c) {
 
 template <int BITS, int PI>
 __global__ __launch_bounds__(kThreads, 1) void project_kernel(ProjectArgs p) {
-  __shared__ __attribute__((aligned(16))) ProjectLds lds;
+  // one LDS array per stage, so that the compiler tracks each stage's loads on its own
+  __shared__ __attribute__((aligned(1024))) __half st0[kStageH];
+  __shared__ __attribute__((aligned(1024))) __half st1[kStageH];
+  __shared__ __attribute__((aligned(1024))) __half st2[kStageH];
+  __shared__ __attribute__((aligned(1024))) __half st3[kStageH];
   const CacheView& c = p.c;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -95,104 +110,108 @@ __global__ __launch_bounds__(kThreads, 1) void project_kernel(ProjectArgs p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
   const int nk = p.hidden / kBK;
-  // piece c = tid + 512 i of a 256 x 64 tile: row c / 8, halves 8 (c % 8) .. + 8; the
-  // byte offsets are 32-bit per-lane values next to wave-uniform bases
   const int rows_valid = min(kBM, p.len - t0);
   const int wrows_valid = min(kBN, nrows - ntile * kBN);
-  uint32_t e_off[kPieces], w_off[kPieces];
-  int lds_off[kPieces];
+  // Direct-to-LDS loads: wave w fills 1-KB pieces q = kDma w + i of a stage (16 staged
+  // rows each; waves 0-3 the E rows, 4-7 the W rows), lane l row 16 q + l / 4 at chunk
+  // slot l % 4.  Rows past the sequence (or the last head) read the last valid row.
+  const bool wave_e = wave < kThreads / 128;
+  const uint8_t* gbase = wave_e ? reinterpret_cast<const uint8_t*>(e_rows) : reinterpret_cast<const uint8_t*>(w_rows);
+  uint32_t goff[kDma];
 #pragma unroll
-  for (int i = 0; i < kPieces; ++i) {
-    const int cpc = tid + kThreads * i, row = cpc >> 3, part = cpc & 7;
-    // rows of E past the sequence (and of W past the last head) read the last valid row
-    // (they are computed, never stored)
-    e_off[i] = (uint32_t)((min(row, rows_valid - 1) * p.hidden + 8 * part) * 2);
-    w_off[i] = (uint32_t)((min(row, wrows_valid - 1) * p.hidden + 8 * part) * 2);
-    lds_off[i] = row * kRowH + 8 * part;
+  for (int i = 0; i < kDma; ++i) {
+    const int r = 16 * (kDma * wave + i) + (lane >> 2);  // staged row 0 .. 511
+    const int row = wave_e ? min(r, rows_valid - 1) : min(r - kBM, wrows_valid - 1);
+    goff[i] = (uint32_t)((row * p.hidden + 8 * stage_chunk(r, lane & 3)) * 2);
   }
-  const uint8_t* e_base = reinterpret_cast<const uint8_t*>(e_rows);
-  const uint8_t* w_base = reinterpret_cast<const uint8_t*>(w_rows);
-  u32x4 ra[kPieces], rb[kPieces];
+  auto load_stage = [&](__half* st, int k) __attribute__((always_inline)) {
+    const uint32_t kb = (uint32_t)(k * kBK * 2);
 #pragma unroll
-  for (int i = 0; i < kPieces; ++i) {
-    ra[i] = *reinterpret_cast<const u32x4*>(e_base + e_off[i]);
-    rb[i] = *reinterpret_cast<const u32x4*>(w_base + w_off[i]);
-  }
-#pragma unroll
-  for (int i = 0; i < kPieces; ++i) {
-    *reinterpret_cast<u32x4*>(&lds.st.a[0][0][0] + lds_off[i]) = ra[i];
-    *reinterpret_cast<u32x4*>(&lds.st.b[0][0][0] + lds_off[i]) = rb[i];
-  }
-  __syncthreads();
-  const int frow = lane & 31, fk = 8 * (lane >> 5);
-  for (int ks = 0; ks < nk; ++ks) {
-    const int buf = ks & 1;
-    const bool more = ks + 1 < nk;
-    if (more) {
-      const uint32_t kb = (uint32_t)((ks + 1) * kBK * 2);
-#pragma unroll
-      for (int i = 0; i < kPieces; ++i) {
-        ra[i] = *reinterpret_cast<const u32x4*>(e_base + e_off[i] + kb);
-        rb[i] = *reinterpret_cast<const u32x4*>(w_base + w_off[i] + kb);
-      }
-    }
-    const __half* sa = &lds.st.a[buf][0][0];
-    const __half* sb = &lds.st.b[buf][0][0];
+    for (int i = 0; i < kDma; ++i)
+      dma16(gbase + goff[i] + kb, (uint32_t)(uintptr_t)(lvoid*)(st + 512 * (kDma * wave + i)));
+  };
+  // fragment reads: lane l reads staged row (base + l % 32), chunk 2 kk + l / 32
+  const int frow = lane & 31;
+  auto compute = [&](const __half* st) __attribute__((always_inline)) {
 #pragma unroll
     for (int kk = 0; kk < kBK / 16; ++kk) {
+      const int ck = 2 * kk + (lane >> 5);
       v8h af[4], bf[2];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        af[i] = *reinterpret_cast<const v8h*>(sa + (128 * wm + 32 * i + frow) * kRowH + 16 * kk + fk);
+      for (int i = 0; i < 4; ++i) {
+        const int r = 128 * wm + 32 * i + frow;
+        af[i] = *reinterpret_cast<const v8h*>(st + r * kBK + 8 * stage_chunk(r, ck));
+      }
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
-        bf[j] = *reinterpret_cast<const v8h*>(sb + (64 * wn + 32 * j + frow) * kRowH + 16 * kk + fk);
+      for (int j = 0; j < 2; ++j) {
+        const int r = kBM + 64 * wn + 32 * j + frow;
+        bf[j] = *reinterpret_cast<const v8h*>(st + r * kBK + 8 * stage_chunk(r, ck));
+      }
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j) acc[i][j] = mfma_f16(af[i], bf[j], acc[i][j]);
     }
-    if (more) {
-      __half* da = &lds.st.a[buf ^ 1][0][0];
-      __half* db = &lds.st.b[buf ^ 1][0][0];
-#pragma unroll
-      for (int i = 0; i < kPieces; ++i) {
-        *reinterpret_cast<u32x4*>(da + lds_off[i]) = ra[i];
-        *reinterpret_cast<u32x4*>(db + lds_off[i]) = rb[i];
-      }
-    }
-    __syncthreads();
+  };
+  // step k: wait for this wave's loads of stage k (the loads of steps k + 1 and k + 2
+  // may stay in flight), barrier (every wave's loads of stage k are in LDS, and every
+  // wave is done with step k - 1, whose stage takes step k + 3), then compute
+  auto step = [&](int k, const __half* cur, __half* nxt) __attribute__((always_inline)) {
+    if (k + 2 < nk) __builtin_amdgcn_s_waitcnt(0x0F70 | (2 * kDma));
+    else if (k + 1 < nk) __builtin_amdgcn_s_waitcnt(0x0F70 | kDma);
+    else __builtin_amdgcn_s_waitcnt(0x0F70);
+    stage_barrier();
+    if (k + 3 < nk) load_stage(nxt, k + 3);
+    compute(cur);
+  };
+  load_stage(st0, 0);
+  if (nk > 1) load_stage(st1, 1);
+  if (nk > 2) load_stage(st2, 2);
+  for (int ks = 0; ks < nk; ks += kStages) {
+    step(ks, st0, st3);
+    if (ks + 1 < nk) step(ks + 1, st1, st0);
+    if (ks + 2 < nk) step(ks + 2, st2, st1);
+    if (ks + 3 < nk) step(ks + 3, st3, st2);
   }
+  stage_barrier();  // every wave is done reading the stages
 
-  // ---- the tile in fp16 (round to nearest even), [token][channel] ----
+  // ---- the tile in fp16 (round to nearest even): head hh's rows 0-127 in stage array
+  // 2 hh, rows 128-255 in 2 hh + 1, 128 channels per row ----
   // accumulator register r of lane l: row 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32
+  {
+    const int a = 2 * (wn >> 1) + wm;
+    __half* dst = a == 0 ? st0 : (a == 1 ? st1 : (a == 2 ? st2 : st3));
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+      for (int j = 0; j < 2; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = 128 * wm + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        const int col = 64 * wn + 32 * j + (lane & 31);
-        lds.tile[row][col] = __float2half_rn(acc[i][j][r]);
-      }
+        for (int r = 0; r < 16; ++r) {
+          const int row = 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+          const int col = 64 * (wn & 1) + 32 * j + (lane & 31);
+          dst[row * 128 + col] = __float2half_rn(acc[i][j][r]);
+        }
+  }
   __syncthreads();
-
   const int valid = rows_valid;
   const int Hq = p.q_heads, H = p.kv_heads;
   constexpr int D = 128, P = D / PI;
 #pragma unroll 1
   for (int hh = 0; hh < 2; ++hh) {
     const int head = 2 * ntile + hh;  // output head: query heads, then key heads, then value heads
-    const int cb = D * hh;            // its channels in the tile
     if (head >= p.nheads) break;
+    const __half* t_lo = hh == 0 ? st0 : st2;
+    const __half* t_hi = hh == 0 ? st1 : st3;
+    auto tile_row = [&](int row) __attribute__((always_inline)) -> const __half* {
+      return (row < 128 ? t_lo : t_hi) + (row & 127) * 128;
+    };
     if (head < Hq) {
       // query head: 128-channel fp16 rows, 16 bytes per thread and step
       __half* dst = p.q + (((int64_t)s * Hq + head) * p.len + t0) * D;
       for (int i = tid; i < valid * (D / 8); i += kThreads) {
         const int row = i / (D / 8), part = i % (D / 8);
         *reinterpret_cast<uint4*>(dst + (int64_t)row * D + 8 * part) =
-            *reinterpret_cast<const uint4*>(&lds.tile[row][cb + 8 * part]);
+            *reinterpret_cast<const uint4*>(tile_row(row) + 8 * part);
       }
     } else if (head < Hq + H) {
       // key head: one thread per (token, partition along the head dimension)
@@ -202,7 +221,7 @@ __global__ __launch_bounds__(kThreads, 1) void project_kernel(ProjectArgs p) {
         float x[PI];
 #pragma unroll
         for (int e = 0; e < PI; e += 8) {
-          const uint4 raw = *reinterpret_cast<const uint4*>(&lds.tile[row][cb + pp * PI + e]);
+          const uint4 raw = *reinterpret_cast<const uint4*>(tile_row(row) + pp * PI + e);
           const __half2* h2 = reinterpret_cast<const __half2*>(&raw);
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
@@ -233,7 +252,7 @@ __global__ __launch_bounds__(kThreads, 1) void project_kernel(ProjectArgs p) {
         const int n = blk < F ? PI : T;
         float x[PI];
 #pragma unroll
-        for (int e = 0; e < PI; ++e) x[e] = e < n ? __half2float(lds.tile[bl * PI + e][cb + ch]) : 0.0f;
+        for (int e = 0; e < PI; ++e) x[e] = e < n ? __half2float(tile_row(bl * PI + e)[ch]) : 0.0f;
         uint32_t w[(PI * BITS + 31) / 32];
         uint16_t mb, sb;
         const uint32_t sum = quantize_values<BITS, PI>(x, n, p.stochastic != 0, p.key_v,
@@ -244,7 +263,7 @@ __global__ __launch_bounds__(kThreads, 1) void project_kernel(ProjectArgs p) {
         store_sum(c.v_sums, vb * D + ch, c.sum_bytes, sum);
         if (blk == F) {
           __half* tail = c.v_tail + (((int64_t)s * H + h) * PI) * D + ch;
-          for (int e = 0; e < T; ++e) tail[(int64_t)e * D] = lds.tile[bl * PI + e][cb + ch];
+          for (int e = 0; e < T; ++e) tail[(int64_t)e * D] = tile_row(bl * PI + e)[ch];
         }
       }
     }
