@@ -475,7 +475,8 @@ def main():
         print(json.dumps({"prefill_from_embeddings": bench_prefill_embeddings(args.prefill_iters)}), flush=True)
         return
     if args.only == "llama8b":
-        print(json.dumps({"decode_llama8b_l4096": bench_llama8b(args.steps, args.warmup, args.replicas)[0]}), flush=True)
+        r, q = bench_llama8b(args.steps, args.warmup, args.replicas)
+        print(json.dumps({"decode_llama8b_l4096": r, "quantize": q}), flush=True)
         return
     if args.only == "long":
         print(json.dumps({"decode_long_l131072": bench_long()}), flush=True)

@@ -1,8 +1,11 @@
 // Quantize-on-write kernels (Sec. 5.1 steps 2 and 9; Sec. 5.2 quantizer; Sec. 5.3
 // partitioning and the fp16 open V block).
-//   quantize_k: one thread per (sequence, kv head, token, K partition along d)
-//   quantize_v: one thread per (sequence, kv head, V block, channel pair)
-//   append    : one workgroup per sequence, one new token for every kv head
+//   quantize_kv: one launch for K and V at partitions below 64: its first workgroups
+//                take one thread per (sequence, kv head, V block, channel pair), the
+//                rest one thread per (sequence, kv head, token, K partition along d),
+//                so the V tasks' serial chains overlap the K tasks' streaming
+//   quantize_k_split / quantize_v_split: partitions of 64 or more, split over lanes
+//   append     : one workgroup per sequence, one new token for every kv head
 // All are HBM-bound: they read fp16 values once and write codes, (min, scale) and sums.
 #include <type_traits>
 
@@ -10,13 +13,13 @@
 
 namespace hack {
 
+// K task gid: (sequence, kv head, token, partition) in row-major order.
 template <int BITS, int PI>
-__global__ __launch_bounds__(256) void quantize_k_kernel(CacheView c, const __half* __restrict__ k,
-                                                         const int32_t* __restrict__ lens, int batch,
-                                                         int max_len, int stochastic, uint64_t key) {
+__device__ __forceinline__ void quantize_k_task(const CacheView& c, const __half* __restrict__ k,
+                                                const int32_t* __restrict__ lens, int batch, int max_len,
+                                                int stochastic, uint64_t key, int64_t gid) {
   const int P = c.head_dim / PI;
   const int64_t total = (int64_t)batch * c.kv_heads * max_len * P;
-  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (gid >= total) return;
   const int p = (int)(gid % P);
   int64_t r = gid / P;
@@ -124,15 +127,15 @@ __global__ __launch_bounds__(256) void quantize_k_split_kernel(CacheView c, cons
 // block's channel pairs are consecutive, so each of the block's PI token rows is
 // read as one contiguous run of 4-byte loads (a whole row per 64 pairs), and each
 // thread writes the adjacent codes, (min, scale) and sums of its two channels.
+// V task gid: (sequence, kv head, V block, channel pair) in row-major order.
 template <int BITS, int PI>
-__global__ __launch_bounds__(256) void quantize_v_kernel(CacheView c, const __half* __restrict__ v,
-                                                         const int32_t* __restrict__ lens, int batch,
-                                                         int max_len, int stochastic, uint64_t key) {
+__device__ __forceinline__ void quantize_v_task(const CacheView& c, const __half* __restrict__ v,
+                                                const int32_t* __restrict__ lens, int batch, int max_len,
+                                                int stochastic, uint64_t key, int64_t gid) {
   constexpr int CB = PI * BITS / 8;  // code bytes per (block, channel)
   const int d = c.head_dim, pairs = d / 2;
   const int NB = (max_len + PI - 1) / PI;
   const int64_t total = (int64_t)batch * c.kv_heads * NB * pairs;
-  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (gid >= total) return;
   const int ch = 2 * (int)(gid % pairs);
   int64_t r = gid / pairs;
@@ -193,6 +196,20 @@ __global__ __launch_bounds__(256) void quantize_v_kernel(CacheView c, const __ha
     for (int e = 0; e < PI; ++e)
       if (e < T) *reinterpret_cast<uint32_t*>(tail + (int64_t)e * d) = raw[e];
   }
+}
+
+// K and V in one launch: workgroups [0, v_blocks) run V tasks, the rest K tasks.
+template <int BITS, int PI>
+__global__ __launch_bounds__(256) void quantize_kv_kernel(CacheView c, const __half* __restrict__ k,
+                                                          const __half* __restrict__ v,
+                                                          const int32_t* __restrict__ lens, int batch, int max_len,
+                                                          int stochastic, uint64_t key_k, uint64_t key_v,
+                                                          int64_t v_blocks) {
+  const int64_t b = blockIdx.x;
+  if (b < v_blocks)
+    quantize_v_task<BITS, PI>(c, v, lens, batch, max_len, stochastic, key_v, b * 256 + threadIdx.x);
+  else
+    quantize_k_task<BITS, PI>(c, k, lens, batch, max_len, stochastic, key_k, (b - v_blocks) * 256 + threadIdx.x);
 }
 
 // V for partitions of 64 tokens or more: one workgroup per (sequence, kv head, V
@@ -371,28 +388,23 @@ static hipError_t quantize_impl(const hack_kv_layout& lay, const CacheView& c, c
                                 hipStream_t stream) {
   const int stoch = lay.rounding == HACK_ROUND_STOCHASTIC;
   const int64_t nk = (int64_t)batch * c.kv_heads * max_len * (c.head_dim / PI);
-  bool k_done = false;
-  if constexpr (PI >= 64) {  // two lanes per partition
-    if (nk > 0) {
+  const int64_t nblk = (int64_t)batch * c.kv_heads * ((max_len + PI - 1) / PI);
+  if constexpr (PI >= 64) {
+    // K: two lanes per partition; V: one workgroup per V block (head_dim <= 256 threads)
+    if (nblk > 0x7FFFFFFF || (2 * nk + 255) / 256 > 0x7FFFFFFF) return hipErrorInvalidValue;
+    if (nk > 0)
       hipLaunchKernelGGL((quantize_k_split_kernel<BITS, PI>), dim3((unsigned)((2 * nk + 255) / 256)), dim3(256), 0,
                          stream, c, k, lens, batch, max_len, stoch, stream_key(lay.seed, 1));
-    }
-    k_done = true;
-  }
-  if (nk > 0 && !k_done)
-    hipLaunchKernelGGL((quantize_k_kernel<BITS, PI>), dim3((unsigned)((nk + 255) / 256)), dim3(256), 0,
-                       stream, c, k, lens, batch, max_len, stoch, stream_key(lay.seed, 1));
-  const int64_t nv = (int64_t)batch * c.kv_heads * ((max_len + PI - 1) / PI) * (c.head_dim / 2);
-  const int64_t nblk = (int64_t)batch * c.kv_heads * ((max_len + PI - 1) / PI);
-  if constexpr (PI >= 64) {  // one workgroup per V block (head_dim <= 256 threads)
-    if (nblk > 0x7FFFFFFF) return hipErrorInvalidValue;
     if (nblk > 0)
       hipLaunchKernelGGL((quantize_v_split_kernel<BITS, PI>), dim3((unsigned)nblk), dim3(c.head_dim), 0, stream, c,
                          v, lens, max_len, stoch, stream_key(lay.seed, 2));
   } else {
-    if (nv > 0)
-      hipLaunchKernelGGL((quantize_v_kernel<BITS, PI>), dim3((unsigned)((nv + 255) / 256)), dim3(256), 0,
-                         stream, c, v, lens, batch, max_len, stoch, stream_key(lay.seed, 2));
+    const int64_t nv = nblk * (c.head_dim / 2);
+    const int64_t vb = (nv + 255) / 256, kb = (nk + 255) / 256;
+    if (vb + kb > 0x7FFFFFFF) return hipErrorInvalidValue;
+    if (vb + kb > 0)
+      hipLaunchKernelGGL((quantize_kv_kernel<BITS, PI>), dim3((unsigned)(vb + kb)), dim3(256), 0, stream, c, k, v,
+                         lens, batch, max_len, stoch, stream_key(lay.seed, 1), stream_key(lay.seed, 2), vb);
   }
   return hipGetLastError();
 }
