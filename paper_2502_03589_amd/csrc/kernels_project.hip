@@ -51,12 +51,16 @@ typedef __attribute__((address_space(3))) void lvoid;
 // reads, eight lanes per cycle) cover all eight 16-byte slots of 128 bytes.
 __device__ __forceinline__ int stage_chunk(int r, int c) { return c ^ ((r >> 1) & 3); }
 
-// 16 bytes per lane from global memory straight into LDS: lane l writes LDS bytes
-// lds + 16 l (lds wave-uniform, via M0).  Issued as inline assembly so that the
-// compiler does not add waits for it before LDS reads of other stages; the kernel
-// waits for each stage's loads explicitly (vmcnt) before the barrier that publishes it.
-__device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
+// 16 bytes per lane from global memory straight into LDS: lane l reads base + off and
+// writes LDS bytes lds + 16 l (base and lds wave-uniform, lds via M0).  Issued as inline
+// assembly so that the compiler does not add waits for it before LDS reads of other
+// stages; the kernel waits for each stage's loads explicitly (vmcnt) before the barrier
+// that publishes it.  The per-lane offset is a register that stays live for the whole
+// main loop, so no later instruction (in particular no matrix-core result) overwrites
+// an address operand while a load is still in flight.
+__device__ __forceinline__ void dma16(const void* base, uint32_t off, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "s"(lds)
+               : "memory", "m0");
 }
 
 // Workgroup barrier that orders LDS accesses without waiting for outstanding
@@ -125,10 +129,9 @@ __global__ __launch_bounds__(kThreads, 1) void project_kernel(ProjectArgs p) {
     goff[i] = (uint32_t)((row * p.hidden + 8 * stage_chunk(r, lane & 3)) * 2);
   }
   auto load_stage = [&](__half* st, int k) __attribute__((always_inline)) {
-    const uint32_t kb = (uint32_t)(k * kBK * 2);
+    const uint8_t* base = gbase + (int64_t)k * kBK * 2;
 #pragma unroll
-    for (int i = 0; i < kDma; ++i)
-      dma16(gbase + goff[i] + kb, (uint32_t)(uintptr_t)(lvoid*)(st + 512 * (kDma * wave + i)));
+    for (int i = 0; i < kDma; ++i) dma16(base, goff[i], (uint32_t)(uintptr_t)(lvoid*)(st + 512 * (kDma * wave + i)));
   };
   // fragment reads: lane l reads staged row (base + l % 32), chunk 2 kk + l / 32
   const int frow = lane & 31;
