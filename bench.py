@@ -619,7 +619,8 @@ def bench_prefill_embeddings(iters: int):
             "attend_ms": round(a_ms, 4), "total_ms": round(p_ms + a_ms, 4), "project_flops": flops,
             "roofline": {"bound": "mfma", "kernel": "project_kernel (QKV GEMM + quantize-on-write)",
                          "achieved": round(tf, 2), "peak": 2500.0, "unit": "TFLOP/s (fp16)",
-                         "frac": round(tf / 2500.0, 4), "traffic": None}}
+                         "frac": round(tf / 2500.0, 4),
+                         "traffic": profiled_traffic("kernels_project.hip", "project_l8192_h4096_hbm_counters.txt")}}
 
 
 def bench_workload(name: str, steps: int, warmup: int):
