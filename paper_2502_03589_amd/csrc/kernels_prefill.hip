@@ -14,16 +14,20 @@
 //            tokens 4g..4g+3 of the tile for row n.  Eq. 4: the rank-1 terms
 //            (m~_q s_k sum k' + R m_k, all partitions) are outer products of a
 //            token-side and a row-side vector, so one v_mfma_f32_16x16x4_f32 per
-//            tile forms them in the tile's layout; the VALU applies s_q s_k to each
-//            converted integer product.  (Moving the scale products or the P'V'
-//            rank-1 terms onto f32 MFMAs too was measured slower: a 16x16x4 f32
-//            MFMA costs more matrix-core time than the VALU work it replaces.)
+//            tile forms them in the tile's layout (its four k slots: two partitions
+//            x two terms); the VALU applies s_q s_k to each converted integer
+//            product.  (The scale products as fp16 matrix-core products of exact
+//            pieces left the time unchanged: the multiplies they remove came back
+//            as operand assembly.)
 //   softmax  online per row with a lazily raised reference max; causal mask.
 //   P        8-bit per (row, V block) with round-to-nearest-even codes; the masked
 //            zeros inside the diagonal block are quantized with it.  The lane's codes
 //            are already the B operand of the P.V product (no transpose).
 //   O^T = V'^T P'^T  one MFMA per (16-channel tile, row tile); an all-ones A gives
-//            the P code sums; Eq. 4 with the cached V sums on the VALU.
+//            the P code sums.  Eq. 4: the VALU applies s_p s_v to each converted
+//            integer product; the rank-1 terms of two V blocks share one
+//            v_mfma_f32_16x16x4_f32 per 16 channels (k slots: two blocks x two
+//            terms, against the cached V sums and minima).
 //   open block  (len mod PI tokens) multiplied in fp16 with unquantized p.
 #include <type_traits>
 
