@@ -59,17 +59,21 @@ def quantize_bytes(B: int, H: int, L: int, d: int, bits: int, pi: int, sum_bytes
     return B * H * (2 * L * d * 2 + decode_bytes_per_seq_head(L, d, bits, pi, sum_bytes))
 
 
-def time_quantize(hk, lay, cache, k, v, lens, L, iters: int = 5):
-    """Median duration (ms) of hack_quantize on the current stream, HIP events around each call."""
+def time_quantize(hk, lay, cache, k, v, lens, L, iters: int = 5, calls: int = 10):
+    """Per-call duration (ms) of hack_quantize: the median over `iters` groups of `calls`
+    back-to-back calls on the current stream (HIP events around each group; every call
+    rewrites the same cache), so one call's launch latency is not counted as its work."""
     import torch
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    hk.hack_quantize(lay, cache, k, v, lens, L)
     ts = []
     for _ in range(iters):
         e0.record()
-        hk.hack_quantize(lay, cache, k, v, lens, L)
+        for _ in range(calls):
+            hk.hack_quantize(lay, cache, k, v, lens, L)
         e1.record()
         torch.cuda.synchronize()
-        ts.append(e0.elapsed_time(e1))
+        ts.append(e0.elapsed_time(e1) / calls)
     return float(np.median(ts))
 
 
