@@ -298,6 +298,7 @@ template <int BITS, int PI, int GT>
 struct WaveLds {
   static constexpr int HT = 4 * GT;
   int8_t p[GT][4][4][PI];       // P codes - qoff: [row tile][block][head][token position]
+  int8_t pz[PI];                // zeros: the P operand of the lanes off the block diagonal
   float pst[GT][4][2][4];       // [rt][block][s_p | m~_p][head], scaled to the span's reference max
   float alpha[GT][4];           // O rescale of the span, per head
   float tailf[GT][4];           // scale of the fp16 open block's probabilities
@@ -467,6 +468,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
   const int F = L / PI, T = L - F * PI;
   const bool requant = a.tail_requant != 0;
   WaveLds<BITS, PI, GT>& wl = wl_all[wave];
+  if (lane < PI / 4) reinterpret_cast<int*>(wl.pz)[lane] = 0;  // read by this wave only
 
   // ---- Q: 8-bit codes per partition with float32 metadata (Sec. 5.1, Sec. 5.2) ----
   // wave w quantizes head slots w, w+4, ...; each lane holds two channels
@@ -649,7 +651,7 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
         load_words<KW>(b.kc + o_kc + ti * 16 * KROW, d.kc[ti]);
         d.km[ti] = *reinterpret_cast<const uint32_t*>(b.km + o_km + ti * 16 * P * 4);
         if constexpr (!SE) d.kz[ti] = 0u;
-        else if constexpr (SB == 1) d.kz[ti] = b.kz[o_kz + ti * 16 * P];
+        else if constexpr (SB == 1) d.kz[ti] = *(b.kz + o_kz + ti * 16 * P);  // offset folds into the load
         else d.kz[ti] = *reinterpret_cast<const uint16_t*>(b.kz + o_kz + ti * 16 * P * 2);
       } else {
 #pragma unroll
@@ -904,18 +906,33 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
       float psp[GT][4], pc1[GT][4], pmt[GT][4];
 #pragma unroll
       for (int rt = 0; rt < GT; ++rt) {
+        // block-diagonal P operand.  At 2 bits the lanes off the diagonal read the zero
+        // row, so every lane loads unconditionally (no masked loads and operand copies);
+        // at 4 bits the kernels sit at the 168-register budget of three waves per SIMD,
+        // which that form exceeds by two registers.
+        if constexpr (BITS == 2) {
+          const int8_t* prow = kk == grp ? &wl.p[rt][kk][hh][0] : &wl.pz[0];
 #pragma unroll
-        for (int sl = 0; sl < TILES; ++sl) {
-          if (kk == grp) {
-            const int4 w = *reinterpret_cast<const int4*>(&wl.p[rt][kk][hh][sl * 16]);
+          for (int sl = 0; sl < TILES; ++sl) {
+            const int4 w = *reinterpret_cast<const int4*>(prow + sl * 16);
             pa[rt][sl] = v4i{w.x, w.y, w.z, w.w};
-          } else {
-            pa[rt][sl] = v4i{0, 0, 0, 0};
+          }
+        } else {
+#pragma unroll
+          for (int sl = 0; sl < TILES; ++sl) {
+            if (kk == grp) {
+              const int4 w = *reinterpret_cast<const int4*>(&wl.p[rt][kk][hh][sl * 16]);
+              pa[rt][sl] = v4i{w.x, w.y, w.z, w.w};
+            } else {
+              pa[rt][sl] = v4i{0, 0, 0, 0};
+            }
           }
         }
         if constexpr (MODE != MODE_PV) {
-          const float4 al = *reinterpret_cast<const float4*>(&wl.alpha[rt][0]);
-          if (al.x != 1.0f || al.y != 1.0f || al.z != 1.0f || al.w != 1.0f) {
+          // the rescale is exactly 1 for a head whose reference max stayed put in this
+          // span; a wave-wide vote skips the multiplies (and the LDS read) when all did
+          if (__builtin_amdgcn_ballot_w64(m_start[rt] != m_ref[rt]) != 0) {
+            const float4 al = *reinterpret_cast<const float4*>(&wl.alpha[rt][0]);
 #pragma unroll
             for (int j = 0; j < 8; ++j) o_acc[rt][j] *= v4f{al.x, al.y, al.z, al.w};
           }
