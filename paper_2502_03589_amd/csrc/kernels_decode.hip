@@ -260,7 +260,11 @@ __device__ __forceinline__ SpanBase span_base(const CacheView& c, int s, int hkv
   int slot0;
   if (c.block_table) {
     const int pidx = span0 / c.page_tokens;
-    const int64_t pg = c.block_table[(int64_t)s * c.mbps + pidx];
+    // the entry is wave-uniform and the kernel never writes the table: a scalar load
+    // through the constant address space, which waits on itself alone (a vector load
+    // here would be followed by a wait on every outstanding vector load)
+    const auto* bt = (const __attribute__((address_space(4))) int32_t*)(uintptr_t)c.block_table;
+    const int64_t pg = bt[(int64_t)s * c.mbps + pidx];
     page = pg < 0 ? 0 : (pg >= c.num_pages ? c.num_pages - 1 : pg);
     slot0 = span0 - pidx * c.page_tokens;
   } else {
