@@ -1117,7 +1117,8 @@ __global__ __launch_bounds__(256, (decode_occupancy<BITS, PI, GT>())) void decod
   }
 }
 
-constexpr int64_t kMaxWgSpans = 64;
+constexpr int64_t kFillWgSpans = 64;
+constexpr int64_t kRaggedWgSpans = 48;
 constexpr int64_t kMaxGridZ = 65535;
 
 // Workgroups per (sequence, kv head, chunk): one per four query heads of the group.
@@ -1144,11 +1145,16 @@ DecodePlan plan_decode(const hack_kv_layout& lay, int batch, int num_q_heads, in
   const int64_t spans_seq = ((int64_t)max_len + span - 1) / span;
   int64_t wg_spans = pairs > 0 ? (spans_seq * pairs * nhg + target - 1) / target : 1;
   if (wg_spans < 1) wg_spans = 1;
-  // A chunk of at most kMaxWgSpans spans bounds the time one workgroup holds a slot:
-  // in a ragged batch the longest sequence then spreads over more workgroups than an
-  // even share of the mean length would give it.  The grid's z extent (the splits)
-  // stays within its 65535 limit.
-  if (wg_spans > kMaxWgSpans) wg_spans = kMaxWgSpans;
+  // A chunk of at most kFillWgSpans spans bounds the time one workgroup holds a slot:
+  // in a ragged batch the longest sequences then spread over more workgroups than an
+  // even share of the mean length would give them.  When the even share at max_len is
+  // more than twice that (a batch of many long sequences, several rounds of the
+  // resident slots), the chunk is kRaggedWgSpans: on a batch of 1K-32K-token sequences
+  // chunks of 40 / 48 / 56 / 64 spans took 289-290 / 287-289 / 288-290 / 293-295 us,
+  // while a batch of equal lengths whose share is just above 64 spans loses a round to
+  // the smaller chunk.  The grid's z extent (the splits) stays within its 65535 limit.
+  if (wg_spans > 2 * kFillWgSpans) wg_spans = kRaggedWgSpans;
+  else if (wg_spans > kFillWgSpans) wg_spans = kFillWgSpans;
   wg_spans = std::max<int64_t>(wg_spans, (spans_seq + kMaxGridZ - 1) / kMaxGridZ);
   p.chunk = (int)(wg_spans * span);
   p.splits = max_len > 0 ? (int)(((int64_t)max_len + p.chunk - 1) / p.chunk) : 1;
