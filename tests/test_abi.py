@@ -175,6 +175,32 @@ def test_workspace_grows_with_context(lib):
     assert 0 < big <= 8 * 65535 * 4 * (4 + 128) * 4 + 4096
 
 
+def _planned_splits(ws, pairs, group, head_groups, head_dim=128):
+    """Chunks per sequence of a decode plan, read back from its workspace size
+    (counters first, 256-byte aligned, then one record of max, sum and O per chunk
+    and query head)."""
+    counters = (pairs * head_groups * 4 + 255) // 256 * 256
+    per_split = pairs * group * (4 + head_dim) * 4
+    records = ws - counters
+    assert records % per_split == 0
+    return records // per_split
+
+
+@pytest.mark.parametrize("bits,batch,hq,max_len,splits", [
+    (2, 64, 64, 32769, 6),    # ragged 70B-shaped batch: even share 343 spans -> chunks of 48 spans
+    (4, 4, 32, 131136, 17),   # long context at 4 bits: share 65 spans -> chunks of 64 (one round)
+    (2, 4, 32, 131136, 24),   # long context at 2 bits: share 43 spans kept
+])
+def test_decode_chunk_plan(lib, bits, batch, hq, max_len, splits):
+    """Split-K chunking of decode: an even share of the resident workgroup slots at
+    max_len, at most 64 spans of 4 partitions (128 tokens at partition 32), and 48 spans
+    when the share exceeds 128 spans (a batch of many long sequences)."""
+    lay = hk.hack_kv_layout_make(128, 8, bits, 32, 256)
+    ws = hk.hack_decode_workspace_bytes(lay, batch, hq, max_len)
+    pairs, group = batch * 8, hq // 8
+    assert _planned_splits(ws, pairs, group, (group + 3) // 4) == splits
+
+
 def test_status_strings(lib):
     for st in range(6):
         assert len(hk.hack_status_string(st)) > 0
